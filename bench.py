@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Benchmark of the W4A4 group-quantized linear on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10]
+
+One step is one pass of the whole hot path over one batch: the per-token,
+per-group SymQuant of fp16 activations x [M, K] (apex4_quantize_act) followed
+by the W4A4 group GEMM against offline-quantized weights (apex4_w4a4_gemm),
+both enqueued on one stream -- apex4_w4a4_linear.  Workload: the paper's
+compute-bound GEMM shape M=2048, N=K=8192, G=128 (APEX4 Fig. 1 / Sec. 5.3 use
+N=K=8192), synthetic seeded data, inputs resident in HBM before timing.
+The inputs are rotated over several copies (> 2x the 256 MB Infinity Cache).
+
+Printed JSON line (rank 0): the metric is TOPS = 2 M N K / t_step; it also
+carries the GEMM kernel's roofline (live HIP-event timing of the GEMM launches
+inside the timed region), the fp16 hipBLASLt GEMM of the same shape, and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5033.2     # MI355X dense INT8 MFMA: 256 CU x 8192 op/clk x 2.4 GHz
+FP16_PEAK_TFLOPS = 2516.6   # MI355X dense FP16 MFMA
+HBM_PEAK_GBS = 8000.0
+
+M, N, K, G = 2048, 8192, 8192, 128
+ROTATE_BYTES = 512 << 20
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
+    return p.parse_args()
+
+
+def traffic_from_profile():
+    """HBM bytes per GEMM launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "gemm_w4a4_paper_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_08761_amd", "csrc", "gemm_w4a4.hip")
+    try:
+        with open(path) as f:
+            prof = json.load(f)
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if prof.get("kernel_source_sha256") != sha:
+            return None
+        return float(prof["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(target_s: float):
+    """The oracle (quantize the sampled activation rows + binary64 GEMM rows)
+    timed on this host for a bounded row sample; TOPS scaled to 2 * rows * N * K."""
+    from oracle import oracle as O
+    from paper_2606_08761_amd import workloads as wl
+
+    x, w = wl.float_workload("paper", M, N, K)
+    Wq, sw = O.quantize(w, G)                       # weights are quantized offline
+    rows = 2
+    while True:
+        t0 = time.perf_counter()
+        Aq, sa = O.quantize(x[:rows], G)
+        O.gemm_rows(Aq, sa, Wq, sw, K, G)
+        dt = time.perf_counter() - t0
+        if dt >= target_s / 2 or rows >= M:
+            break
+        rows = min(M, max(rows * 2, int(rows * target_s / max(dt, 1e-3) / 2)))
+    reps = 1
+    while dt * reps < target_s and reps < 8:       # repeat the whole-M sample up to the target
+        t0 = time.perf_counter()
+        Aq, sa = O.quantize(x[:rows], G)
+        O.gemm_rows(Aq, sa, Wq, sw, K, G)
+        dt = (dt * reps + time.perf_counter() - t0) / (reps + 1)
+        reps += 1
+    tops = 2.0 * rows * N * K / dt / 1e12
+    return {"value": tops, "unit": "TOPS", "cores": O.num_threads(), "kind": "oracle",
+            "sample": f"{rows} of {M} rows of the M={M} N={N} K={K} G={G} linear "
+                      f"(quantize rows + int64/fp64 GEMM rows), mean of {reps} run(s) of {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
+              "(the multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+
+    # ---- inputs: fp16 activations and offline-quantized weights, R rotating copies ----
+    x_h, w_h = wl.float_workload("paper", M, N, K)
+    per_set = M * K * 2 + N * K // 2 + N * (K // G) * 2 + M * N * 2 + M * K // 2 + M * (K // G) * 2
+    R = max(2, -(-ROTATE_BYTES // per_set))
+    sets = []
+    w_dev = torch.from_numpy(w_h).to(dev)
+    Wq0, sw0 = pk.apex4_quantize_act(w_dev, G)
+    for r in range(R):
+        x = torch.from_numpy(x_h).to(dev)
+        if r:
+            x = x.roll(r, dims=0).contiguous()           # different bytes per set, same distribution
+        sets.append(dict(x=x, Wq=Wq0.clone(), sw=sw0.clone(),
+                         Y=torch.empty((M, N), dtype=torch.float16, device=dev),
+                         Aq=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                         sa=torch.empty((M, K // G), dtype=torch.float16, device=dev)))
+    del w_dev
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        s = sets[i % R]
+        if ev is not None:
+            ev[0].record(stream)
+        pk.apex4_quantize_act(s["x"], G, s["Aq"], s["sa"])
+        if ev is not None:
+            ev[1].record(stream)
+        pk.apex4_w4a4_gemm(s["Aq"], s["sa"], s["Wq"], s["sw"], G, s["Y"])
+        if ev is not None:
+            ev[2].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly `steps` steps ----
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    quant_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_per_step = wall * 1e3 / args.steps
+    ops = 2.0 * M * N * K
+    value = ops / (ms_per_step * 1e-3) / 1e12
+    gemm_tops = ops / (gemm_ms * 1e-3) / 1e12
+
+    # ---- GEMM alone on the random-code workload (value-independent speed check) ----
+    Aq_h, sa_h, Wq_h, sw_h = wl.codes_workload("paper", M, N, K, G)
+    c = [torch.from_numpy(a).to(dev) for a in (Aq_h, sa_h, Wq_h, sw_h)]
+    Yc = torch.empty((M, N), dtype=torch.float16, device=dev)
+    for _ in range(5):
+        pk.apex4_w4a4_gemm(*c, G, Yc)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    e0.record(stream)
+    for _ in range(reps):
+        pk.apex4_w4a4_gemm(*c, G, Yc)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    codes_gemm_ms = e0.elapsed_time(e1) / reps
+    del c, Yc
+
+    # ---- fp16 GEMM of the same shape (torch -> hipBLASLt), rotated too ----
+    fsets = []
+    Rf = max(2, -(-ROTATE_BYTES // (M * K * 2 + N * K * 2 + M * N * 2)))
+    wf = torch.from_numpy(w_h).to(dev)
+    for r in range(Rf):
+        fsets.append((torch.from_numpy(x_h).to(dev), wf.clone(), torch.empty((M, N), dtype=torch.float16, device=dev)))
+    for i in range(5):
+        xf, wff, yf = fsets[i % Rf]
+        torch.matmul(xf, wff.t(), out=yf)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(reps):
+        xf, wff, yf = fsets[i % Rf]
+        torch.matmul(xf, wff.t(), out=yf)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fp16_ms = e0.elapsed_time(e1) / reps
+    del fsets, wf
+
+    line = {
+        "metric": "W4A4-g128 GEMM TOPS + speedup vs fp16 GEMM, M=2048 N=K=8192; % INT8 MFMA peak",
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": "W4A4-g128 linear, paper GEMM shape: quantize fp16 x[2048,8192] "
+                               "(SymQuant, G=128) + W4A4 GEMM against W_q[8192,8192]",
+                   "M": M, "N": N, "K": K, "G": G, "parallelism": "none (1 GPU)",
+                   "mfma": "v_mfma_i32_32x32x32_i8, i32 group sums, fp32 dequant, fp16 out",
+                   "rotating_input_sets": R},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
+                     "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": traffic_from_profile(), "kernel": "w4a4_gemm_kernel",
+                     "kernel_us": round(gemm_ms * 1e3, 3)},
+        "quant_us": round(quant_ms * 1e3, 3),
+        "quant_hbm_gbs": round((2.5 * M * K + 2 * M * K / G) / (quant_ms * 1e-3) / 1e9, 1),
+        "gemm_us": round(gemm_ms * 1e3, 3),
+        "gemm_tops": round(gemm_tops, 2),
+        "gemm_pct_int8_peak": round(100 * gemm_tops / INT8_PEAK_TOPS, 2),
+        "gemm_random_codes_us": round(codes_gemm_ms * 1e3, 3),
+        "fp16_gemm_us": round(fp16_ms * 1e3, 3),
+        "fp16_gemm_tflops": round(ops / (fp16_ms * 1e-3) / 1e12, 2),
+        "speedup_gemm_vs_fp16": round(fp16_ms / gemm_ms, 3),
+        "speedup_step_vs_fp16": round(fp16_ms / ms_per_step, 3),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

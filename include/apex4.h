@@ -1,0 +1,129 @@
+/*
+ * apex4.h -- C ABI of the MI355X (gfx950) W4A4 group-quantized GEMM library.
+ *
+ * Method: APEX4, "Efficient Pure W4A4 LLM Inference via Intra-SM Compute
+ * Rebalancing" (arXiv 2606.08761).
+ *
+ * Data formats (shared by every entry point):
+ *   - binary16 buffers are passed as void* and hold IEEE 754 binary16 bit
+ *     patterns (torch.float16);
+ *   - packed 4-bit codes are uint8 [rows, K/2], row-major, two signed codes in
+ *     [-8, 7] per byte along K, low nibble = even k (Sec. 4.4 stores activations
+ *     and weights as packed 4-bit vectors; this library packs both along K);
+ *   - scales are binary16 [rows, K/G], row-major: one per row and K-group
+ *     (Sec. 4.4: S1 for activations, S2 for weights, both FP16);
+ *   - Y = A W^T: A_q is [M, K/2], W_q is [N, K/2] (nn.Linear layout), Y is
+ *     binary16 [M, N], row-major.
+ *
+ * Ownership and execution: every pointer is caller-owned device memory.  The
+ * library never allocates, frees, synchronises or keeps a pointer past the
+ * call.  Outputs are fully overwritten; inputs and outputs must not alias.
+ * Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and is
+ * complete once that stream is synchronised.  Calls are reentrant.
+ *
+ * Errors: every entry point returns an apex4_status and never prints or
+ * aborts.  Arguments are validated before any HIP call, in this order:
+ * NULL pointers, shapes, group size, alignment, device; M == 0 is a
+ * successful no-op (after validation), and buffers whose size is zero
+ * (M-sized when M == 0, the group-sum dump when mr == 0) may be NULL.  A failed launch returns
+ * APEX4_ERR_LAUNCH.  Nothing is written when validation fails.
+ *
+ * Shape rules:  M >= 0, N >= 1, K >= 128 and K % 128 == 0, K % G == 0.
+ * Group sizes: the GEMM takes G in {128, 256, 512} or G == K (per-channel,
+ * Sec. 3.2.2); the quantizer takes any G with G % 32 == 0 and K % G == 0.
+ * Alignment: every pointer 16-byte aligned.
+ * Device: the current device must be gfx950 (MI355X / MI350X).
+ */
+#ifndef APEX4_H
+#define APEX4_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    APEX4_OK = 0,
+    APEX4_ERR_NULL = -1,    /* a required pointer is NULL */
+    APEX4_ERR_SHAPE = -2,   /* M, N, K or a row window out of range */
+    APEX4_ERR_GROUP = -3,   /* unsupported group size G */
+    APEX4_ERR_ALIGN = -4,   /* a pointer is not 16-byte aligned */
+    APEX4_ERR_LAUNCH = -5,  /* the HIP launch failed */
+    APEX4_ERR_DEVICE = -6   /* no device, or the current device is not gfx950 */
+} apex4_status;
+
+/*
+ * Per-token, per-group activation quantizer (SymQuant with b = 4).
+ * Sec. 3.2.1, Eq. (SymQuant): S_g = max|X_g| / 7, X_g^q = clamp(round(X_g/S_g), -8, 7);
+ * applied online to activations (Sec. 4.4) and offline to weights (Alg. 1).
+ *
+ *   x    [M, K] binary16 input (device).
+ *   A_q  [M, K/2] packed codes (device, output).
+ *   s_a  [M, K/G] binary16 scales (device, output).
+ *
+ * Per (row, group): amax = max|x|; S = the binary16 nearest to amax/7 (ties to
+ * even); codes = clamp(round-half-even(x / S), -8, 7), taken on the exact
+ * quotient; a group whose S is zero gets zero codes.  Bit-exact and
+ * deterministic.  The same call quantizes weights ([N, K] -> W_q, s_w).
+ */
+int apex4_quantize_act(const void* x, int64_t M, int64_t K, int64_t G,
+                       uint8_t* A_q, void* s_a, void* stream);
+
+/*
+ * Pure W4A4 group-quantized GEMM.
+ * Sec. 3.2.1, Eq. (group_decomposition): C = sum_g (A_g^q W_g^q) (.) (S_g^a S_g^w^T);
+ * Sec. 4.2: immediate per-group dequantization (groups) and delayed
+ * dequantization (per-channel, G == K).
+ *
+ *   A_q [M, K/2] codes, s_a [M, K/G] scales, W_q [N, K/2] codes, s_w [N, K/G]
+ *   scales (all device, read-only);  Y [M, N] binary16 (device, output).
+ *
+ *   Y[m,n] = binary16( sum_g s_a[m,g] s_w[n,g] P[m,n,g] ),
+ *   P[m,n,g] = sum_{k in g} A_q[m,k] W_q[n,k]  (exact 32-bit integer sums).
+ * The scaled sum is accumulated in binary32; the result is rounded once to
+ * binary16 (round to nearest even).
+ */
+int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a,
+                    const uint8_t* W_q, const void* s_w,
+                    int64_t M, int64_t N, int64_t K, int64_t G,
+                    void* Y, void* stream);
+
+/*
+ * Debug form of apex4_w4a4_gemm: the exact integer group sums of Eq.
+ * (group_decomposition), produced by the same GEMM kernel with a dump epilogue
+ * in place of the dequantization.
+ *
+ *   P [mr, N, K/G] int32 (device, output): P[i, n, g] for rows m0 + i,
+ *   0 <= m0, 0 <= mr, m0 + mr <= M.
+ */
+int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
+                              int64_t M, int64_t N, int64_t K, int64_t G,
+                              int64_t m0, int64_t mr, int32_t* P, void* stream);
+
+/*
+ * Quantize-then-GEMM linear layer: the inference forward of one quantized
+ * linear layer (Sec. 3.2.1: activations quantized dynamically, weights
+ * offline).  Enqueues apex4_quantize_act(x) into the caller's work buffers
+ * and then apex4_w4a4_gemm on the same stream.
+ *
+ *   x [M, K] binary16, W_q [N, K/2], s_w [N, K/G]  (device, read-only);
+ *   Y [M, N] binary16 (device, output);
+ *   A_q_work [M, K/2] and s_a_work [M, K/G] (device, caller-owned scratch,
+ *   overwritten with the quantized activations).
+ */
+int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
+                      int64_t M, int64_t N, int64_t K, int64_t G,
+                      void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* apex4_status_string(int status);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int apex4_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APEX4_H */

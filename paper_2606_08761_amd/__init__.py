@@ -1,1 +1,151 @@
-"""MI355X-native W4A4 group-quantized GEMM (APEX4 hot path) -- Python binding."""
+"""MI355X-native W4A4 group-quantized GEMM (the hot path of APEX4, arXiv 2606.08761).
+
+Thin Python binding over the C ABI in ``include/apex4.h`` (``libapex4.so``).
+The functions carry the C names and only marshal arguments: torch supplies
+device memory and the stream, every step of the computation runs in the HIP
+kernels.  There is no fallback: if the library is missing or the device is
+not gfx950 the call raises.
+
+    A_q, s_a = apex4_quantize_act(x, G)                 # x: [M, K] float16 on cuda
+    Y = apex4_w4a4_gemm(A_q, s_a, W_q, s_w, G)          # Y: [M, N] float16
+    P = apex4_w4a4_gemm_groupsums(A_q, W_q, G, m0, mr)  # int32 [mr, N, K/G]
+    Y = apex4_w4a4_linear(x, W_q, s_w, G)               # quantize + GEMM
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libapex4.so")
+
+APEX4_OK = 0
+STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
+          -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}
+
+EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
+            "apex4_w4a4_linear", "apex4_status_string", "apex4_version")
+
+_lib = None
+
+
+class Apex4Error(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {msg}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded ``libapex4.so`` with its argument types declared."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2606_08761_amd.build` (no fallback path exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I = ctypes.c_void_p, ctypes.c_int64
+    L.apex4_quantize_act.argtypes = [P, I, I, I, P, P, P]
+    L.apex4_w4a4_gemm.argtypes = [P, P, P, P, I, I, I, I, P, P]
+    L.apex4_w4a4_gemm_groupsums.argtypes = [P, P, I, I, I, I, I, I, P, P]
+    L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
+    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear"):
+        getattr(L, f).restype = ctypes.c_int
+    L.apex4_status_string.argtypes = [ctypes.c_int]
+    L.apex4_status_string.restype = ctypes.c_char_p
+    L.apex4_version.argtypes = []
+    L.apex4_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(fn: str, rc: int):
+    if rc != APEX4_OK:
+        raise Apex4Error(fn, rc, lib().apex4_status_string(rc).decode())
+
+
+def _stream(t, stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(t.device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def apex4_quantize_act(x, G: int, A_q=None, s_a=None, stream=None):
+    """SymQuant (b=4) of a [M, K] float16 tensor in groups of G along K.
+
+    Returns (A_q uint8 [M, K/2], s_a float16 [M, K/G])."""
+    import torch
+    M, K = x.shape
+    if A_q is None:
+        A_q = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if s_a is None:
+        s_a = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
+    rc = lib().apex4_quantize_act(_dev(x, torch.float16, "x"), M, K, G, _dev(A_q, torch.uint8, "A_q"),
+                                  _dev(s_a, torch.float16, "s_a"), _stream(x, stream))
+    _check("apex4_quantize_act", rc)
+    return A_q, s_a
+
+
+def apex4_w4a4_gemm(A_q, s_a, W_q, s_w, G: int, Y=None, stream=None):
+    """Y[M, N] = sum_g s_a[:, g] s_w[:, g]^T (.) (A_q,g W_q,g^T), float16 output."""
+    import torch
+    M, K2 = A_q.shape
+    N = W_q.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
+    rc = lib().apex4_w4a4_gemm(_dev(A_q, torch.uint8, "A_q"), _dev(s_a, torch.float16, "s_a"),
+                               _dev(W_q, torch.uint8, "W_q"), _dev(s_w, torch.float16, "s_w"),
+                               M, N, 2 * K2, G, _dev(Y, torch.float16, "Y"), _stream(A_q, stream))
+    _check("apex4_w4a4_gemm", rc)
+    return Y
+
+
+def apex4_w4a4_gemm_groupsums(A_q, W_q, G: int, m0: int = 0, mr: int | None = None, P=None, stream=None):
+    """Exact int32 group sums P[i, n, g] for rows m0 .. m0+mr-1 (debug dump)."""
+    import torch
+    M, K2 = A_q.shape
+    N, K = W_q.shape[0], 2 * K2
+    if mr is None:
+        mr = M - m0
+    if P is None:
+        P = torch.empty((mr, N, max(K // G, 1)), dtype=torch.int32, device=A_q.device)
+    rc = lib().apex4_w4a4_gemm_groupsums(_dev(A_q, torch.uint8, "A_q"), _dev(W_q, torch.uint8, "W_q"),
+                                         M, N, K, G, m0, mr, _dev(P, torch.int32, "P"),
+                                         _stream(A_q, stream))
+    _check("apex4_w4a4_gemm_groupsums", rc)
+    return P
+
+
+def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None, stream=None):
+    """Quantize x (SymQuant) then the W4A4 GEMM, both enqueued on one stream."""
+    import torch
+    M, K = x.shape
+    N = W_q.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    if A_q_work is None:
+        A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if s_a_work is None:
+        s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
+    rc = lib().apex4_w4a4_linear(_dev(x, torch.float16, "x"), _dev(W_q, torch.uint8, "W_q"),
+                                 _dev(s_w, torch.float16, "s_w"), M, N, K, G,
+                                 _dev(Y, torch.float16, "Y"), _dev(A_q_work, torch.uint8, "A_q_work"),
+                                 _dev(s_a_work, torch.float16, "s_a_work"), _stream(x, stream))
+    _check("apex4_w4a4_linear", rc)
+    return Y
+
+
+def apex4_version() -> int:
+    return int(lib().apex4_version())

@@ -1,0 +1,20 @@
+// Internal launcher interface between the C ABI front end (api.hip) and the
+// kernel translation units.  Arguments are already validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace apex4 {
+
+// Activation/weight quantizer (SymQuant, b = 4).
+hipError_t launch_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t G,
+                           uint8_t* q, uint16_t* s, hipStream_t stream);
+
+// W4A4 GEMM.  When P is non-null the kernel dumps the exact integer group sums
+// of rows [0, M) of the given operands instead of dequantizing (Y unused).
+hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
+                       const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
+                       uint16_t* Y, int32_t* P, hipStream_t stream);
+
+}  // namespace apex4

@@ -1,0 +1,157 @@
+// C ABI front end: argument validation (before any HIP call), device check and
+// dispatch to the kernel launchers.  See include/apex4.h for the contract.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "apex4.h"
+#include "apex4_internal.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+// 0 = unknown, 1 = gfx950, -1 = other architecture.
+std::atomic<int> g_arch_ok[kMaxDevices];
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return APEX4_ERR_DEVICE;
+    if (dev < kMaxDevices) {
+        const int known = g_arch_ok[dev].load(std::memory_order_relaxed);
+        if (known == 1) return APEX4_OK;
+        if (known == -1) return APEX4_ERR_DEVICE;
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return APEX4_ERR_DEVICE;
+    const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (dev < kMaxDevices) g_arch_ok[dev].store(ok ? 1 : -1, std::memory_order_relaxed);
+    return ok ? APEX4_OK : APEX4_ERR_DEVICE;
+}
+
+// Shape rules shared by the GEMM entry points.
+int check_gemm_shape(int64_t M, int64_t N, int64_t K) {
+    if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    return APEX4_OK;
+}
+
+int check_gemm_group(int64_t K, int64_t G) {
+    if (G <= 0) return APEX4_ERR_GROUP;
+    if (G == K) return APEX4_OK;
+    if (G != 128 && G != 256 && G != 512) return APEX4_ERR_GROUP;
+    if (K % G != 0) return APEX4_ERR_SHAPE;
+    return APEX4_OK;
+}
+
+// Buffers sized by M (or by a row window) may be NULL when that size is zero.
+bool present(const void* p, int64_t rows) { return p != nullptr || rows == 0; }
+
+int check_quant_args(const void* x, int64_t M, int64_t K, int64_t G, const void* A_q, const void* s_a) {
+    if (!present(x, M) || !present(A_q, M) || !present(s_a, M)) return APEX4_ERR_NULL;
+    if (M < 0 || K < 128 || (K % 128) != 0 || M > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (G <= 0 || (G % 32) != 0 || G > K) return APEX4_ERR_GROUP;
+    if (K % G != 0) return APEX4_ERR_SHAPE;
+    if (!aligned16(x) || !aligned16(A_q) || !aligned16(s_a)) return APEX4_ERR_ALIGN;
+    return APEX4_OK;
+}
+
+int check_gemm_args(const void* A_q, const void* s_a, const void* W_q, const void* s_w, int64_t M,
+                    int64_t N, int64_t K, int64_t G, const void* Y) {
+    if (!present(A_q, M) || !present(s_a, M) || !W_q || !s_w || !present(Y, M)) return APEX4_ERR_NULL;
+    int rc = check_gemm_shape(M, N, K);
+    if (rc) return rc;
+    rc = check_gemm_group(K, G);
+    if (rc) return rc;
+    if (!aligned16(A_q) || !aligned16(s_a) || !aligned16(W_q) || !aligned16(s_w) || !aligned16(Y))
+        return APEX4_ERR_ALIGN;
+    return APEX4_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* apex4_status_string(int status) {
+    switch (status) {
+        case APEX4_OK: return "APEX4_OK";
+        case APEX4_ERR_NULL: return "APEX4_ERR_NULL: a required pointer is NULL";
+        case APEX4_ERR_SHAPE: return "APEX4_ERR_SHAPE: M, N, K or the row window is out of range";
+        case APEX4_ERR_GROUP: return "APEX4_ERR_GROUP: unsupported group size";
+        case APEX4_ERR_ALIGN: return "APEX4_ERR_ALIGN: a pointer is not 16-byte aligned";
+        case APEX4_ERR_LAUNCH: return "APEX4_ERR_LAUNCH: kernel launch failed";
+        case APEX4_ERR_DEVICE: return "APEX4_ERR_DEVICE: no gfx950 device is current";
+        default: return "APEX4: unknown status";
+    }
+}
+
+int apex4_version(void) { return 100; }
+
+int apex4_quantize_act(const void* x, int64_t M, int64_t K, int64_t G, uint8_t* A_q, void* s_a,
+                       void* stream) {
+    int rc = check_quant_args(x, M, K, G, A_q, s_a);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    hipError_t e = apex4::launch_quantize(static_cast<const uint16_t*>(x), M, K, G, A_q,
+                                          static_cast<uint16_t*>(s_a), static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
+                    int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+    int rc = check_gemm_args(A_q, s_a, W_q, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    hipError_t e = apex4::launch_gemm(A_q, static_cast<const uint16_t*>(s_a), W_q,
+                                      static_cast<const uint16_t*>(s_w), M, N, K, G, static_cast<uint16_t*>(Y),
+                                      nullptr, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M, int64_t N, int64_t K,
+                              int64_t G, int64_t m0, int64_t mr, int32_t* P, void* stream) {
+    if (!present(A_q, M) || !W_q || !present(P, mr)) return APEX4_ERR_NULL;
+    int rc = check_gemm_shape(M, N, K);
+    if (rc) return rc;
+    rc = check_gemm_group(K, G);
+    if (rc) return rc;
+    if (m0 < 0 || mr < 0 || m0 > M || mr > M - m0) return APEX4_ERR_SHAPE;
+    const uint8_t* A_win = A_q + m0 * (K / 2);
+    if (!aligned16(A_q) || !aligned16(W_q) || !aligned16(P) || !aligned16(A_win)) return APEX4_ERR_ALIGN;
+    rc = check_device();
+    if (rc) return rc;
+    if (mr == 0) return APEX4_OK;
+    hipError_t e = apex4::launch_gemm(A_win, nullptr, W_q, nullptr, mr, N, K, G, nullptr, P,
+                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
+                      int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, void* stream) {
+    if (!present(x, M) || !W_q || !s_w || !present(Y, M) || !present(A_q_work, M) || !present(s_a_work, M))
+        return APEX4_ERR_NULL;
+    int rc = check_gemm_args(A_q_work, s_a_work, W_q, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    rc = check_quant_args(x, M, K, G, A_q_work, s_a_work);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = apex4::launch_quantize(static_cast<const uint16_t*>(x), M, K, G, A_q_work,
+                                          static_cast<uint16_t*>(s_a_work), st);
+    if (e != hipSuccess) return APEX4_ERR_LAUNCH;
+    e = apex4::launch_gemm(A_q_work, static_cast<const uint16_t*>(s_a_work), W_q,
+                           static_cast<const uint16_t*>(s_w), M, N, K, G, static_cast<uint16_t*>(Y), nullptr,
+                           st);
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+}  // extern "C"

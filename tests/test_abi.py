@@ -1,0 +1,165 @@
+"""Host-side checks of the C ABI (no GPU needed, no kernel launched).
+
+  * libapex4.so loads and exports every function include/apex4.h declares;
+  * argument validation returns the documented status codes before any HIP
+    call (pointers passed here are host addresses that must never be touched);
+  * the Python binding refuses non-device tensors instead of falling back.
+"""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "apex4.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2606_08761_amd as pk
+    if not os.path.exists(pk.LIB_PATH):
+        from paper_2606_08761_amd import build
+        build.build()
+    return pk.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(apex4_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
+              "apex4_w4a4_linear", "apex4_status_string", "apex4_version"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    import paper_2606_08761_amd as pk
+    out = subprocess.run(["nm", "-D", "--defined-only", pk.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(re.findall(r"\bT (apex4_\w+)", out.stdout))
+    for f in declared_functions():
+        assert f in exported, f
+        assert hasattr(L, f)
+    assert set(pk.EXPORTED) <= exported
+
+
+def test_status_strings(L):
+    for code, name in {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
+                       -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}.items():
+        assert L.apex4_status_string(code).decode().startswith(name)
+    assert L.apex4_status_string(12345)
+    assert L.apex4_version() >= 100
+
+
+class Host:
+    """16-byte aligned host buffers whose addresses stand in for device pointers.
+    Validation fails before anything dereferences them."""
+
+    def __init__(self):
+        self.buf = np.zeros(4096, np.uint8)
+        base = self.buf.ctypes.data
+        self.p = (base + 15) & ~15
+
+    def ptr(self, off=0):
+        return ctypes.c_void_p(self.p + off)
+
+
+NULL = ctypes.c_void_p(0)
+
+
+def test_quantize_validation(L):
+    h = Host()
+    q = L.apex4_quantize_act
+    s = NULL
+    assert q(NULL, 4, 256, 128, h.ptr(), h.ptr(), s) == -1
+    assert q(h.ptr(), 4, 256, 128, NULL, h.ptr(), s) == -1
+    assert q(h.ptr(), 4, 256, 128, h.ptr(), NULL, s) == -1
+    assert q(h.ptr(), -1, 256, 128, h.ptr(), h.ptr(), s) == -2
+    assert q(h.ptr(), 4, 96, 32, h.ptr(), h.ptr(), s) == -2        # K % 128
+    assert q(h.ptr(), 4, 0, 128, h.ptr(), h.ptr(), s) == -2
+    assert q(h.ptr(), 4, 256, 48, h.ptr(), h.ptr(), s) == -3       # G % 32
+    assert q(h.ptr(), 4, 256, 512, h.ptr(), h.ptr(), s) == -3      # G > K
+    assert q(h.ptr(), 4, 384, 256, h.ptr(), h.ptr(), s) == -2      # K % G
+    assert q(h.ptr(), 4, 256, 0, h.ptr(), h.ptr(), s) == -3
+    assert q(h.ptr(8), 4, 256, 128, h.ptr(), h.ptr(), s) == -4
+    assert q(h.ptr(), 4, 256, 128, h.ptr(2), h.ptr(), s) == -4
+    assert q(h.ptr(), 4, 256, 128, h.ptr(), h.ptr(4), s) == -4
+
+
+def test_gemm_validation(L):
+    h = Host()
+    g = L.apex4_w4a4_gemm
+    s = NULL
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -1
+    assert g(*ok, 4, 8, 256, 128, NULL, s) == -1
+    assert g(*ok, -1, 8, 256, 128, h.ptr(), s) == -2
+    assert g(*ok, 4, 0, 256, 128, h.ptr(), s) == -2
+    assert g(*ok, 4, 8, 64, 64, h.ptr(), s) == -2                  # K < 128
+    assert g(*ok, 4, 8, 320, 64, h.ptr(), s) == -2                 # K % 128
+    assert g(*ok, 4, 8, 256, 64, h.ptr(), s) == -3                 # G not in {128,256,512,K}
+    assert g(*ok, 4, 8, 1024, 1000, h.ptr(), s) == -3
+    assert g(*ok, 4, 8, 384, 256, h.ptr(), s) == -2                # K % G
+    assert g(h.ptr(1), *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -4
+    assert g(*ok, 4, 8, 256, 128, h.ptr(2), s) == -4
+
+
+def test_groupsums_validation(L):
+    h = Host()
+    f = L.apex4_w4a4_gemm_groupsums
+    s = NULL
+    assert f(NULL, h.ptr(), 8, 8, 256, 128, 0, 8, h.ptr(), s) == -1
+    assert f(h.ptr(), h.ptr(), 8, 8, 256, 128, 0, 8, NULL, s) == -1
+    assert f(h.ptr(), h.ptr(), 8, 8, 256, 128, 4, 5, h.ptr(), s) == -2   # window past M
+    assert f(h.ptr(), h.ptr(), 8, 8, 256, 128, -1, 2, h.ptr(), s) == -2
+    assert f(h.ptr(), h.ptr(), 8, 8, 256, 96, 0, 8, h.ptr(), s) == -3
+    assert f(h.ptr(), h.ptr(), 8, 8, 256, 128, 0, 8, h.ptr(4), s) == -4
+
+
+def test_linear_validation(L):
+    h = Host()
+    f = L.apex4_w4a4_linear
+    s = NULL
+    args = lambda **kw: [kw.get(k, h.ptr()) for k in ("x", "wq", "sw")]
+    assert f(*args(x=NULL), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -1
+    assert f(*args(), 4, 8, 256, 128, h.ptr(), NULL, h.ptr(), s) == -1
+    assert f(*args(), 4, 8, 200, 128, h.ptr(), h.ptr(), h.ptr(), s) == -2
+    assert f(*args(), 4, 8, 256, 32, h.ptr(), h.ptr(), h.ptr(), s) == -3
+    assert f(*args(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -4
+
+
+def test_device_check_without_gpu():
+    """Valid arguments on a machine with no gfx950 device: APEX4_ERR_DEVICE, not a crash.
+    Run in a child process so the HIP runtime probe stays out of the test process."""
+    code = r"""
+import ctypes, numpy as np, sys
+sys.path.insert(0, %r)
+import paper_2606_08761_amd as pk
+L = pk.lib()
+b = np.zeros(1 << 16, np.uint8); p = ctypes.c_void_p((b.ctypes.data + 255) & ~255)
+print(L.apex4_w4a4_gemm(p, p, p, p, 0, 8, 256, 128, p, None))
+""" % ROOT
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is visible")
+    except Exception:
+        pass
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "-6"
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    import paper_2606_08761_amd as pk
+    x = torch.zeros((4, 256), dtype=torch.float16)
+    with pytest.raises(TypeError):
+        pk.apex4_quantize_act(x, 128)

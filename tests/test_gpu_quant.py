@@ -1,0 +1,104 @@
+"""GPU parity of the activation/weight quantizer (APEX4 Sec. 3.2.1, Eq. SymQuant).
+
+Codes and scales must be bit-identical to the CPU oracle.  Inputs are seeded
+binary16 activations N(0,1) with 1% outlier channels x20 (the llama70b and
+decode workloads), weights N(0, 0.02), and hand-built edge rows.
+"""
+import numpy as np
+import pytest
+
+from parity import dev, host, log
+from paper_2606_08761_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_quantize(x16: np.ndarray, G: int):
+    import paper_2606_08761_amd as pk
+    q, s = pk.apex4_quantize_act(dev(x16), G)
+    return host(q), host(s)
+
+
+def assert_same(x16, G, O, what):
+    q, s = gpu_quantize(x16, G)
+    qo, so = O.quantize(x16, G)
+    assert np.array_equal(s.view(np.uint16), so.view(np.uint16)), f"{what}: scales differ"
+    assert np.array_equal(q, qo), f"{what}: codes differ"
+
+
+@pytest.mark.parametrize("M,K,G", [
+    (1, 128, 128), (8, 1024, 128), (33, 1024, 32), (64, 1024, 64), (64, 1024, 256),
+    (64, 1024, 512), (64, 1024, 1024), (5, 8192, 8192), (16, 8192, 128), (256, 8192, 128),
+    (16, 28672, 128), (32, 8192, 8192), (3, 28672, 28672), (7, 2048, 1024), (100, 384, 384),
+])
+def test_activations_bit_exact(O, M, K, G):
+    log(f"quantize activations M={M} K={K} G={G}")
+    x, _ = wl.float_workload("decode", M, 128, K)
+    assert_same(x, G, O, f"M={M} K={K} G={G}")
+
+
+@pytest.mark.parametrize("G", [128, 256, 512, 8192])
+def test_large_activation_matrix(O, G):
+    M, K = 4096, 8192
+    log(f"quantize activations M={M} K={K} G={G}")
+    r = wl.rng_for("gsweep", 1, G)
+    x = wl.activations(r, M, K)
+    assert_same(x, G, O, f"gsweep G={G}")
+
+
+def _edge_rows(K: int) -> np.ndarray:
+    u = 2.0 ** -24
+    rows = []
+    rows.append(np.zeros(K))                                   # all zero -> scale 0
+    rows.append(np.full(K, -0.0))                              # negative zeros
+    r = np.zeros(K); r[::7] = 3 * u; r[1::7] = -2 * u; rows.append(r)     # amax 3u -> scale 0
+    r = np.zeros(K); r[::5] = 10 * u; r[2::5] = -10 * u; r[3::5] = 3 * u; rows.append(r)  # clamp to -8 and 7
+    r = np.arange(K) % 2047 * u; rows.append(r)                # subnormal ramp
+    # exact ties: per 32-block, amax = 7 * 2^e and the other values (j + 1/2) 2^e
+    k = np.arange(K)
+    e = np.exp2((k // 32) % 20 - 10)
+    j = (k % 14) - 7
+    r = (j + 0.5) * e
+    r[::32] = 7 * e[::32]
+    rows.append(r)
+    rows.append(np.where(np.arange(K) % 2, 65504.0, -65504.0))  # binary16 extremes
+    r = np.linspace(-1, 1, K); r[::64] = 1e-7; rows.append(r)
+    return np.stack(rows).astype(np.float16)
+
+
+@pytest.mark.parametrize("G", [32, 128, 256, 512, 1024])
+def test_edge_rows(O, G):
+    K = 1024
+    x = _edge_rows(K)
+    log(f"edge rows G={G}")
+    assert_same(x, G, O, f"edge G={G}")
+
+
+def test_weights_full_size_sampled_rows(O):
+    """The gate+up weight of a Llama-2-70B layer, [57344, 8192], quantized on the GPU;
+    a sample of rows is re-quantized by the oracle."""
+    import torch
+    import paper_2606_08761_amd as pk
+    N, K, G = 57344, 8192, 128
+    log("generate gate_up weights")
+    w = wl.weights(wl.rng_for("llama70b", 7), N, K)
+    q, s = pk.apex4_quantize_act(dev(w), G)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 127, 128, 28671, 28672, 57343] + list(np.random.default_rng(1).integers(0, N, 9)))
+    qh, sh = host(q)[rows], host(s)[rows]
+    qo, so = O.quantize(w[rows], G)
+    assert np.array_equal(sh.view(np.uint16), so.view(np.uint16))
+    assert np.array_equal(qh, qo)
+
+
+def test_deterministic_and_m_zero():
+    import torch
+    import paper_2606_08761_amd as pk
+    x, _ = wl.float_workload("decode", 64, 128, 2048)
+    xd = dev(x)
+    q1, s1 = pk.apex4_quantize_act(xd, 128)
+    q2, s2 = pk.apex4_quantize_act(xd, 128)
+    torch.cuda.synchronize()
+    assert torch.equal(q1, q2) and torch.equal(s1, s2)
+    # M == 0 is a successful no-op
+    pk.apex4_quantize_act(torch.empty((0, 2048), dtype=torch.float16, device="cuda"), 128)
