@@ -45,6 +45,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
+    p.add_argument("--mode", choices=("bench", "counters", "rho"), default="bench",
+                   help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
+                        "rho: the intra-CU throughput probes")
     return p.parse_args()
 
 
@@ -94,8 +97,35 @@ def cpu_baseline(target_s: float):
                       f"(quantize rows + int64/fp64 GEMM rows), mean of {reps} run(s) of {dt:.1f} s"}
 
 
+def counters_mode():
+    """Launch the paper-shape GEMM 3 times and a 256 MiB reference copy 3 times,
+    nothing else, so that per-dispatch counters of both can be compared."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import rho, workloads as wl
+    dev = torch.device("cuda", 0)
+    c = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("paper", M, N, K, G)]
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    src = torch.randint(0, 255, (256 << 20,), dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        rho.copy(src, dst)
+    for _ in range(3):
+        pk.apex4_w4a4_gemm(*c, G, Y)
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "counters", "copy_bytes": 256 << 20, "gemm": [M, N, K, G],
+                      "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
+
+
 def main():
     args = parse()
+    if args.mode == "counters":
+        return counters_mode()
+    if args.mode == "rho":
+        from paper_2606_08761_amd import rho
+        print(json.dumps(rho.measure()), flush=True)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
               "(the multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)

@@ -6,24 +6,43 @@
 // dequantization for per-channel scales (Sec. 4.2).
 //
 // CDNA4 mapping
-//   * gfx950 has no 4-bit integer matrix instruction, so the packed nibbles are
-//     widened to int8 MFMA operands.  The widening keeps each nibble in the high
-//     half of its byte: (w << 4) & 0xF0F0F0F0 yields the even-k codes times 16
-//     and w & 0xF0F0F0F0 the odd-k codes times 16 (two VALU ops per 8 codes plus
-//     one).  A and W go through the same widening, so the MFMA sees the same
-//     k permutation on both sides and every group sum comes out exactly
-//     256 * P; the 1/256 is folded into the weight scale (a power of two,
-//     exact).
-//   * v_mfma_i32_32x32x32_i8 accumulates P in int32 per group (exact:
-//     |256 P| <= 256 * 64 * G < 2^31 for G <= 2^16).
-//   * The i32 -> f32 conversion and the s_a * s_w scaling run on the VALU once
-//     per group; for G == K they run once, after the K loop.
-//   * Operands are staged HBM -> registers -> (widen) -> LDS, double-buffered,
-//     so each byte is widened once per workgroup, not once per wave.
-//   * LDS rows are XOR-swizzled in 16-byte chunks so that the 32 rows read by
-//     one MFMA operand fetch hit distinct banks.
-//   * Workgroup ids are remapped so that each XCD (8 per MI355X, separate L2)
-//     works on a contiguous band of output tiles.
+//   * No 4-bit integer matrix instruction exists on gfx950, so packed nibbles
+//     are widened to int8 MFMA operands: (w << 4) & 0xF0F0F0F0 gives the
+//     even-position codes times 16, w & 0xF0F0F0F0 the odd-position codes times
+//     16 (three VALU ops per 8 codes).  A and W are widened the same way, so
+//     every MFMA sums products of matching k and each group sum comes out as
+//     exactly 256 P; the 1/256 is folded into the activation scale (a power of
+//     two, exact).
+//   * v_mfma_i32_32x32x32_i8 accumulates 256 P in int32 per group (exact:
+//     |256 P| <= 2^14 G < 2^31 for G <= 2^16).
+//   * The MFMA is fed W as its first operand and A as its second, so a 32 x 32
+//     result block is Y^T: lane l holds output row m = l % 32 and 16 output
+//     columns.  The activation scale is then one value per lane.
+//   * Dequantization, binary32 on the VALU, once per group and output element.
+//     For G <= 256 the first MFMA of a group starts from the bit pattern of
+//     1.5 * 2^23 instead of 0, so the int32 result read as binary32 is
+//     1.5 * 2^23 + 256 P exactly (|256 P| <= 2^22), and
+//         t   = fma(D, s_a/256, -1.5 * 2^23 * s_a/256)      (= fl(P s_a))
+//         acc = fma(t, s_w, acc)          (s_w binary16 through v_fma_mix_f32)
+//     i.e. two VALU ops with no int -> float conversion.  Larger groups and
+//     per-channel scales use float(D) instead of the bias.
+//   * Staging.  The activation tile is shared by all waves of a workgroup: it
+//     goes HBM -> registers (one stage ahead) -> widen -> LDS (double-buffered,
+//     rows padded to 144 bytes so 8 or 16 consecutive rows at the same chunk
+//     hit distinct banks and every fragment offset is an immediate).  Each
+//     wave owns distinct weight columns, so the weight fragments go straight
+//     from global memory into registers (one stage ahead) and are widened there;
+//     the weights never touch LDS.
+//   * K slots.  In a 128-wide K stage, lane half h of MFMA kk covers
+//     k in [64 h + 16 kk, 64 h + 16 kk + 16): the packed dwords at byte
+//     32 h + 8 kk of the row, widened as even(w0), odd(w0), even(w1), odd(w1).
+//     A lane's weight bytes for a stage are one contiguous 32-byte run.
+//   * Groups.  G == 128: one group per stage, each block's group sum is
+//     dequantized right after its four MFMAs.  G in {256, 512}: group sums
+//     persist over the stages of a group.  G == K: sums persist over all of K
+//     and the scales are applied once in the epilogue.
+//   * Workgroup ids are remapped so that each XCD (8 per MI355X, each with its
+//     own L2) works on a contiguous band of output tiles.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -38,40 +57,62 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;          // output tile rows (M)
-constexpr int BN = 128;          // output tile columns (N)
-constexpr int KS = 128;          // K elements per pipeline stage
-constexpr int ROWB = KS;         // bytes of one widened int8 row in LDS
-constexpr int NTHREADS = 256;    // 4 waves, 2 x 2, each owns a 64 x 64 sub-tile
+constexpr int KS = 128;                       // K elements per pipeline stage
+constexpr int KK = KS / 32;                   // MFMAs per 32 x 32 block per stage
+constexpr int AROW = KS + 16;                 // padded bytes of one widened LDS row
+constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
+constexpr float MAGIC = 12582912.0f;
 
-struct __align__(16) Stage {
-    int8_t a[BM * ROWB];
-    int8_t w[BN * ROWB];
-    float sa[BM];
-    float sw[BN];
+enum Mode : int {
+    kRotate = 0,    // G == 128: one group per stage
+    kPersist = 1,   // G in {256, 512}: group sums persist over the stages of a group
+    kChannel = 2,   // G == K: one scale per row and column, applied in the epilogue
+    kDump = 3,      // exact integer group sums written out (debug)
 };
 
-// Byte offset of 16-byte chunk `chunk` (0..7) of widened row `row`.
-__device__ __forceinline__ int swz(int row, int chunk) {
-    return row * ROWB + ((chunk ^ (row & 7)) << 4);
-}
-
-__device__ __forceinline__ uint4 widen_even(uint4 v) {
-    return make_uint4((v.x << 4) & 0xF0F0F0F0u, (v.y << 4) & 0xF0F0F0F0u, (v.z << 4) & 0xF0F0F0F0u,
-                      (v.w << 4) & 0xF0F0F0F0u);
-}
-__device__ __forceinline__ uint4 widen_odd(uint4 v) {
-    return make_uint4(v.x & 0xF0F0F0F0u, v.y & 0xF0F0F0F0u, v.z & 0xF0F0F0F0u, v.w & 0xF0F0F0F0u);
-}
+template <int BM, int NT>
+struct Stage {
+    int8_t a[BM * AROW];
+    uint16_t scale[NT];   // [0, BM): s_a rows; [BM, BM + BN): s_w columns; rest unused
+};
 
 __device__ __forceinline__ float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+__device__ __forceinline__ uint32_t even_w(uint32_t w) { return (w << 4) & 0xF0F0F0F0u; }
+__device__ __forceinline__ uint32_t odd_w(uint32_t w) { return w & 0xF0F0F0F0u; }
 
-template <bool DUMP>
-__global__ __launch_bounds__(NTHREADS, 2) void w4a4_gemm_kernel(
+// 16 int8 MFMA operand values from two packed dwords (16 codes).
+__device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
+    i32x4 r;
+    r[0] = static_cast<int>(even_w(w0));
+    r[1] = static_cast<int>(odd_w(w0));
+    r[2] = static_cast<int>(even_w(w1));
+    r[3] = static_cast<int>(odd_w(w1));
+    return r;
+}
+
+__device__ __forceinline__ i32x16 splat16(int v) {
+    i32x16 r;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r[i] = v;
+    return r;
+}
+
+// One workgroup computes a BM x BN tile with WAVES_M x WAVES_N waves; each
+// wave owns MI x NJ blocks of 32 x 32 (rows x columns).
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
     int32_t* __restrict__ P) {
-    __shared__ Stage st[2];
+    constexpr int NT = 64 * WAVES_M * WAVES_N;
+    constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
+    constexpr int A_CH = BM * 4 / NT;                 // 16-byte packed activation chunks per thread
+    constexpr bool ROTATE = MODE == kRotate;
+    constexpr bool NEED_ACC = (MODE == kRotate || MODE == kPersist);
+    static_assert(A_CH * NT == BM * 4, "tile / thread mismatch");
+    static_assert(BM + BN <= NT, "one staged scale per thread");
+
+    __shared__ Stage<BM, NT> st[2];
 
     // ---- tile selection (XCD-aware) ----
     const int mt_count = (M + BM - 1) / BM;
@@ -84,172 +125,284 @@ __global__ __launch_bounds__(NTHREADS, 2) void w4a4_gemm_kernel(
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, lh = lane >> 5;
-
-    const int64_t rowbytes = K / 2;
     const int nks = K / KS;
-    const int spg = G / KS;          // pipeline stages per group
+    const int spg = G / KS;           // stages per group
     const int ng = K / G;
 
-    // ---- global -> register prefetch of one stage ----
-    uint4 ra[2], rw[2];
-    uint16_t rs = 0;
-    auto load_stage = [&](int ks) {
+    // ---- per-lane offsets (32-bit); uniform stage bases live in scalar registers.
+    // Rows past M or N are clamped to the last row: they only feed outputs that
+    // are never stored, so loads need no branch.
+    uint32_t a_off[A_CH];
+    int a_lds0[A_CH], a_lds1[A_CH];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int c = tid + i * NTHREADS;
-            const int r = c >> 2, p = c & 3;
-            const int gm = m0 + r, gn = n0 + r;
-            const int64_t koff = static_cast<int64_t>(ks) * (KS / 2) + p * 16;
-            ra[i] = gm < M ? *reinterpret_cast<const uint4*>(Aq + gm * rowbytes + koff) : make_uint4(0, 0, 0, 0);
-            rw[i] = gn < N ? *reinterpret_cast<const uint4*>(Wq + gn * rowbytes + koff) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < A_CH; ++i) {
+        const int c = tid + i * NT;
+        const int r = c >> 2, p = c & 3;
+        a_off[i] = static_cast<uint32_t>(min(m0 + r, M - 1)) * static_cast<uint32_t>(K / 2) + p * 16;
+        // packed dwords 4p .. 4p+3 are lane half p/2, MFMAs 2(p%2) and 2(p%2)+1
+        const int c0 = 2 * (2 * (p & 1)) + (p >> 1);
+        a_lds0[i] = r * AROW + c0 * 16;
+        a_lds1[i] = r * AROW + (c0 + 2) * 16;
+    }
+    // Scale staged by this thread: an activation row, a weight column, or (past
+    // BM + BN) a clamped dummy that is never read.
+    const uint16_t* sc_base;
+    uint32_t sc_off;
+    {
+        const bool is_a = tid < BM;
+        const int row = is_a ? min(m0 + tid, M - 1) : min(n0 + min(tid - BM, BN - 1), N - 1);
+        sc_base = is_a ? sa : sw;
+        sc_off = static_cast<uint32_t>(row) * static_cast<uint32_t>(ng);
+    }
+    uint32_t w_off[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int n = min(n0 + wn * NJ * 32 + j * 32 + l32, N - 1);
+        w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + 32 * lh;
+    }
+
+    uint4 ra[A_CH];
+    uint16_t rsc = 0;
+    auto load_a = [&](int ks) {
+        const uint8_t* base = Aq + static_cast<int64_t>(ks) * (KS / 2);
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
+        if constexpr (MODE != kDump) rsc = (sc_base + ks / spg)[sc_off];
+    };
+    auto store_a = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_CH; ++i) {
+            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0[i]]) = frag2(ra[i].x, ra[i].y);
+            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1[i]]) = frag2(ra[i].z, ra[i].w);
         }
-        if (!DUMP && (ks + 1) % spg == 0) {
-            const int g = ks / spg;
-            if (tid < BM) {
-                const int gm = m0 + tid;
-                rs = gm < M ? sa[static_cast<int64_t>(gm) * ng + g] : 0;
-            } else {
-                const int gn = n0 + tid - BM;
-                rs = gn < N ? sw[static_cast<int64_t>(gn) * ng + g] : 0;
+        if constexpr (MODE != kDump) st[buf].scale[tid] = rsc;
+    };
+    uint4 w[NJ][2];
+    auto load_w = [&](int ks) {
+        const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            w[j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
+            w[j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
+        }
+    };
+
+    f32x16 acc[NEED_ACC ? MI : 1][NEED_ACC ? NJ : 1];
+    if constexpr (NEED_ACC) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    }
+    i32x16 psum[ROTATE ? 1 : MI][ROTATE ? 1 : NJ];
+    const i32x16 start = splat16(MAGIC_OK ? static_cast<int>(MAGIC_BITS) : 0);
+
+    auto read_a = [&](int buf, int i, i32x4 (&af)[KK]) {
+        const int row = wm * MI * 32 + i * 32 + l32;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            af[kk] = *reinterpret_cast<const i32x4*>(&st[buf].a[row * AROW + (2 * kk + lh) * 16]);
+    };
+    // Weight scales of this lane's 16 columns in block j (binary16 pairs).
+    auto read_sw = [&](int buf, int j, uint2 (&swh)[4]) {
+        const int c = BM + wn * NJ * 32 + j * 32 + 4 * lh;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[buf].scale[c + 8 * q]);
+    };
+    // Activation scale of this lane's row in block i, with the 1/256 of the widening.
+    auto read_sa = [&](int buf, int i) {
+        return h2f(st[buf].scale[wm * MI * 32 + i * 32 + l32]) * (1.0f / 256.0f);
+    };
+    auto sw_at = [](const uint2 (&swh)[4], int r) {
+        const uint32_t pair = (r & 2) ? swh[r >> 2].y : swh[r >> 2].x;
+        return (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
+    };
+    // acc += fl(P s_a) * s_w.
+    auto dequant = [&](const i32x16& D, f32x16& a, float sav, const uint2 (&swh)[4]) {
+        const float nb = -MAGIC * sav;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float t;
+            if constexpr (MAGIC_OK) t = fmaf(__int_as_float(D[r]), sav, nb);
+            else t = static_cast<float>(D[r]) * sav;
+            a[r] = fmaf(t, h2f(sw_at(swh, r)), a[r]);
+        }
+    };
+
+    // One K stage: widen this wave's weight fragments, issue the next stage's
+    // weight loads into the freed registers, then run the row blocks.
+    auto compute = [&](int buf, int next, auto FIRST) {
+        constexpr bool group_first = decltype(FIRST)::value;
+        i32x4 bw[NJ][KK];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const uint4& v = w[j][kk >> 1];
+                bw[j][kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
+            }
+        // keep both weight copies from being live at once (register budget)
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(next);
+        __builtin_amdgcn_sched_barrier(0);
+        uint2 swh[ROTATE ? NJ : 1][4];
+        float sav[ROTATE ? MI : 1];
+        if constexpr (ROTATE) {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) read_sw(buf, j, swh[j]);
+#pragma unroll
+            for (int i = 0; i < MI; ++i) sav[i] = read_sa(buf, i);
+        }
+        i32x4 af[2][KK];
+        read_a(buf, 0, af[0]);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            if (i + 1 < MI) read_a(buf, i + 1, af[(i + 1) & 1]);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                i32x16 d;
+                if constexpr (ROTATE || group_first) d = start;
+                else d = psum[i][j];
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk)
+                    d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][kk], af[i & 1][kk], d, 0, 0, 0);
+                if constexpr (ROTATE) dequant(d, acc[i][j], sav[i], swh[j]);
+                else psum[i][j] = d;
             }
         }
     };
-    auto store_stage = [&](int ks, int buf) {
+
+    // End of a group for the persistent modes.
+    auto finish_group = [&](int buf, int g) {
+        if constexpr (MODE == kPersist) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int c = tid + i * NTHREADS;
-            const int r = c >> 2, p = c & 3;
-            *reinterpret_cast<uint4*>(&st[buf].a[swz(r, 2 * p)]) = widen_even(ra[i]);
-            *reinterpret_cast<uint4*>(&st[buf].a[swz(r, 2 * p + 1)]) = widen_odd(ra[i]);
-            *reinterpret_cast<uint4*>(&st[buf].w[swz(r, 2 * p)]) = widen_even(rw[i]);
-            *reinterpret_cast<uint4*>(&st[buf].w[swz(r, 2 * p + 1)]) = widen_odd(rw[i]);
+            for (int j = 0; j < NJ; ++j) {
+                uint2 swh[4];
+                read_sw(buf, j, swh);
+#pragma unroll
+                for (int i = 0; i < MI; ++i) dequant(psum[i][j], acc[i][j], read_sa(buf, i), swh);
+            }
+        } else if constexpr (MODE == kDump) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int gm = m0 + wm * MI * 32 + i * 32 + l32;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                        const int v = MAGIC_OK ? (psum[i][j][r] - static_cast<int>(MAGIC_BITS)) : psum[i][j][r];
+                        if (gm < M && gn < N) P[(static_cast<int64_t>(gm) * N + gn) * ng + g] = v >> 8;
+                    }
+            }
         }
-        if (!DUMP && (ks + 1) % spg == 0) {
-            if (tid < BM) st[buf].sa[tid] = h2f(rs);
-            else st[buf].sw[tid - BM] = h2f(rs) * (1.0f / 256.0f);   // undo the x16 * x16 widening
-        }
+        (void)buf;
+        (void)g;
     };
 
-    i32x16 acc_i[2][2];
-    f32x16 acc_f[2][2];
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) { acc_f[rb][cb][r] = 0.f; acc_i[rb][cb][r] = 0; }
+    // ---- main loop over K.  Stage ks lives in LDS buffer ks & 1.  Loads past the
+    // last stage are clamped to it (harmless re-reads), so the rotating body is
+    // branch-free.
+    auto step = [&](int ks, auto BUF) {
+        constexpr int buf = decltype(BUF)::value;
+        const int ahead = min(ks + 1, nks - 1);
+        load_a(ahead);
+        if constexpr (ROTATE) {
+            compute(buf, ahead, std::true_type{});
+        } else {
+            if ((ks % spg) == 0) compute(buf, ahead, std::true_type{});
+            else compute(buf, ahead, std::false_type{});
+            if (MODE != kChannel && (ks + 1) % spg == 0) finish_group(buf, ks / spg);
+        }
+        store_a(buf ^ 1);
+        __syncthreads();
+    };
+    load_a(0);
+    load_w(0);
+    store_a(0);
+    __syncthreads();
+    int ks = 0;
+    for (; ks + 2 <= nks; ks += 2) {
+        step(ks, std::integral_constant<int, 0>{});
+        step(ks + 1, std::integral_constant<int, 1>{});
+    }
+    if (ks < nks) step(ks, std::integral_constant<int, 0>{});
 
-    auto compute = [&](int buf, auto first_tag) {
-        constexpr bool FIRST = decltype(first_tag)::value;
+    if constexpr (MODE == kDump) return;
+
+    // ---- epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3.
+    // The last step stored a copy of the final stage (and its scales) into the
+    // buffer it did not read, so either buffer holds the final scales.
+    const int lastbuf = nks & 1;
 #pragma unroll
-        for (int kk = 0; kk < KS / 32; ++kk) {
-            i32x4 a[2], b[2];
+    for (int i = 0; i < MI; ++i) {
+        const int gm = m0 + wm * MI * 32 + i * 32 + l32;
+        float sav = 0.f;
+        if constexpr (MODE == kChannel) sav = read_sa(lastbuf, i);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
-                a[rb] = *reinterpret_cast<const i32x4*>(&st[buf].a[swz(wm * 64 + rb * 32 + l32, 2 * kk + lh)]);
+        for (int j = 0; j < NJ; ++j) {
+            uint2 swh[4];
+            if constexpr (MODE == kChannel) read_sw(lastbuf, j, swh);
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-                b[cb] = *reinterpret_cast<const i32x4*>(&st[buf].w[swz(wn * 64 + cb * 32 + l32, 2 * kk + lh)]);
+            for (int q = 0; q < 4; ++q) {
+                float v[4];
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    if (FIRST && kk == 0) {
-                        const i32x16 zero = {};
-                        acc_i[rb][cb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[rb], b[cb], zero, 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 4 * q + e;
+                    if constexpr (MODE == kChannel) v[e] = static_cast<float>(psum[i][j][r]) * sav * h2f(sw_at(swh, r));
+                    else v[e] = acc[i][j][r];
+                }
+                const uint32_t h01 = __half_as_ushort(__float2half_rn(v[0])) |
+                                     (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(v[1]))) << 16);
+                const uint32_t h23 = __half_as_ushort(__float2half_rn(v[2])) |
+                                     (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(v[3]))) << 16);
+                const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * q + 4 * lh;
+                if (gm < M) {
+                    uint16_t* dst = Y + static_cast<int64_t>(gm) * N + gn;
+                    if ((N & 3) == 0 && gn + 3 < N) {
+                        *reinterpret_cast<uint2*>(dst) = make_uint2(h01, h23);
                     } else {
-                        acc_i[rb][cb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[rb], b[cb], acc_i[rb][cb], 0, 0, 0);
+                        if (gn + 0 < N) dst[0] = static_cast<uint16_t>(h01 & 0xFFFFu);
+                        if (gn + 1 < N) dst[1] = static_cast<uint16_t>(h01 >> 16);
+                        if (gn + 2 < N) dst[2] = static_cast<uint16_t>(h23 & 0xFFFFu);
+                        if (gn + 3 < N) dst[3] = static_cast<uint16_t>(h23 >> 16);
                     }
                 }
+            }
         }
-    };
-
-    // Output row (within the 32 x 32 MFMA block) of accumulator element r of this lane.
-    auto out_row = [&](int r) { return 8 * (r >> 2) + 4 * lh + (r & 3); };
-
-    auto dequant = [&](int buf) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const float swv = st[buf].sw[wn * 64 + cb * 32 + l32];
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float sav = st[buf].sa[wm * 64 + rb * 32 + out_row(r)];
-                    acc_f[rb][cb][r] = fmaf(static_cast<float>(acc_i[rb][cb][r]) * swv, sav, acc_f[rb][cb][r]);
-                }
-            }
-    };
-
-    auto dump = [&](int g) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const int gn = n0 + wn * 64 + cb * 32 + l32;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int gm = m0 + wm * 64 + rb * 32 + out_row(r);
-                    if (gm < M && gn < N)
-                        P[(static_cast<int64_t>(gm) * N + gn) * ng + g] = acc_i[rb][cb][r] >> 8;
-                }
-            }
-    };
-
-    // ---- main loop over K ----
-    load_stage(0);
-    store_stage(0, 0);
-    __syncthreads();
-    for (int ks = 0; ks < nks; ++ks) {
-        const int buf = ks & 1;
-        if (ks + 1 < nks) load_stage(ks + 1);
-        if (ks % spg == 0) compute(buf, std::true_type{});
-        else compute(buf, std::false_type{});
-        if ((ks + 1) % spg == 0) {
-            if constexpr (DUMP) dump(ks / spg);
-            else dequant(buf);
-        }
-        if (ks + 1 < nks) store_stage(ks + 1, buf ^ 1);
-        __syncthreads();
     }
+}
 
-    // ---- epilogue: binary32 -> binary16 (RNE) ----
-    if constexpr (!DUMP) {
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const int gn = n0 + wn * 64 + cb * 32 + l32;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int gm = m0 + wm * 64 + rb * 32 + out_row(r);
-                    if (gm < M && gn < N)
-                        Y[static_cast<int64_t>(gm) * N + gn] = __half_as_ushort(__float2half_rn(acc_f[rb][cb][r]));
-                }
-            }
-    }
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK>
+hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+    constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
+    const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK>), dim3(static_cast<unsigned>(tiles)),
+                       dim3(64 * WAVES_M * WAVES_N), 0, stream, Aq, sa, Wq, sw, static_cast<int>(M),
+                       static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
+    return hipGetLastError();
 }
 
 }  // namespace
 
+// Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P,
                        hipStream_t stream) {
-    const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const dim3 grid(static_cast<unsigned>(tiles)), block(NTHREADS);
     if (P) {
-        hipLaunchKernelGGL(w4a4_gemm_kernel<true>, grid, block, 0, stream, Aq, sa, Wq, sw,
-                           static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G),
-                           Y, P);
-    } else {
-        hipLaunchKernelGGL(w4a4_gemm_kernel<false>, grid, block, 0, stream, Aq, sa, Wq, sw,
-                           static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G),
-                           Y, P);
+        if (G <= 256) return launch<1, 8, 4, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+        return launch<1, 8, 4, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     }
-    return hipGetLastError();
+    if (G == K) return launch<1, 8, 4, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 128) return launch<1, 8, 4, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 256) return launch<1, 8, 4, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    return launch<1, 8, 4, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
 }
 
 }  // namespace apex4
