@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -45,9 +46,14 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho"), default="bench",
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize"), default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
-                        "rho: the intra-CU throughput probes")
+                        "rho: the intra-CU throughput probes; "
+                        "summarize: turn rocprofv3 CSV output into the profiles/ summaries")
+    p.add_argument("--fetch-csv", help="summarize: counter_collection.csv of the FETCH_SIZE pass")
+    p.add_argument("--write-csv", help="summarize: counter_collection.csv of the WRITE_SIZE pass")
+    p.add_argument("--stats-csv", help="summarize: kernel_stats.csv of the --kernel-trace --stats run")
+    p.add_argument("--commands", help="summarize: text file with the exact commands that made the CSVs")
     return p.parse_args()
 
 
@@ -97,6 +103,75 @@ def cpu_baseline(target_s: float):
                       f"(quantize rows + int64/fp64 GEMM rows), mean of {reps} run(s) of {dt:.1f} s"}
 
 
+def summarize_mode(args):
+    """profiles/gemm_w4a4_paper_traffic.json and profiles/gemm_w4a4_paper_shape.md from
+    rocprofv3 output.  FETCH_SIZE / WRITE_SIZE (KiB per dispatch) are scaled by
+    what the same counter reads for the 256 MiB reference copy."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r.get("Counter_Name") != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    def pick(vals, key):
+        xs = [v for k, vs in vals.items() if key in k for v in vs]
+        return statistics.mean(xs) if xs else None
+
+    copy_kib = (256 << 20) / 1024.0
+    fetch = per_kernel(args.fetch_csv, "FETCH_SIZE")
+    write = per_kernel(args.write_csv, "WRITE_SIZE")
+    f_copy, w_copy = pick(fetch, "copy_kernel"), pick(write, "copy_kernel")
+    f_gemm, w_gemm = pick(fetch, "w4a4_gemm_kernel"), pick(write, "w4a4_gemm_kernel")
+    f_scale, w_scale = copy_kib / f_copy, copy_kib / w_copy
+    read_b = f_gemm * f_scale * 1024.0
+    write_b = w_gemm * w_scale * 1024.0
+    alg = M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N
+    src = os.path.join(ROOT, "paper_2606_08761_amd", "csrc", "gemm_w4a4.hip")
+    stats = list(csv.DictReader(open(args.stats_csv)))
+    cmds = open(args.commands).read().strip() if args.commands else ""
+    prof = {
+        "kernel": "w4a4_gemm_kernel (G=128 rotating mode)",
+        "workload": f"M={M} N={N} K={K} G={G}",
+        "kernel_source_sha256": hashlib.sha256(open(src, "rb").read()).hexdigest(),
+        "fetch_kib_per_dispatch": f_gemm, "write_kib_per_dispatch": w_gemm,
+        "copy_fetch_kib": f_copy, "copy_write_kib": w_copy, "copy_bytes": 256 << 20,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "hbm_read_bytes_per_launch": read_b, "hbm_write_bytes_per_launch": write_b,
+        "hbm_bytes_per_launch": read_b + write_b,
+        "algorithmic_bytes_per_launch": alg,
+        "commands": cmds,
+    }
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_traffic.json"), "w") as f:
+        json.dump(prof, f, indent=1)
+    lines = ["# W4A4 GEMM, M=2048 N=K=8192 G=128: rocprofv3 summary", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
+             "## Kernel trace (`--kernel-trace --stats`, bench.py default workload)", "",
+             "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:8]:
+        name = r["Name"]
+        m = re.search(r"(\w+_kernel(?:<[^()]*>)?)", name)
+        short = (m.group(1) if m else name.split("(")[0])[:80]
+        lines.append(f"| `{short}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} |")
+    lines += ["", "## HBM traffic of the GEMM (`--pmc FETCH_SIZE`, then `--pmc WRITE_SIZE`, `bench.py --mode counters`)", "",
+              f"* reference copy of 256 MiB: FETCH_SIZE {f_copy:.0f} KiB (scale {f_scale:.3f}), "
+              f"WRITE_SIZE {w_copy:.0f} KiB (scale {w_scale:.3f})",
+              f"* GEMM per dispatch: FETCH_SIZE {f_gemm:.0f} KiB -> {read_b / 1e6:.1f} MB read; "
+              f"WRITE_SIZE {w_gemm:.0f} KiB -> {write_b / 1e6:.1f} MB written",
+              f"* algorithmic bytes per launch: {alg / 1e6:.1f} MB; measured / algorithmic = "
+              f"{(read_b + write_b) / alg:.2f}",
+              f"* kernel source sha256: `{prof['kernel_source_sha256']}`"]
+    with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(prof, indent=1))
+
+
 def counters_mode():
     """Launch the paper-shape GEMM 3 times and a 256 MiB reference copy 3 times,
     nothing else, so that per-dispatch counters of both can be compared."""
@@ -122,6 +197,8 @@ def main():
     args = parse()
     if args.mode == "counters":
         return counters_mode()
+    if args.mode == "summarize":
+        return summarize_mode(args)
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
