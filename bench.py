@@ -45,6 +45,7 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
     p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize"), default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
@@ -193,6 +194,68 @@ def counters_mode():
                       "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
 
 
+DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)]
+
+
+def decode_bench(reps: int = 50):
+    """Decode-size linears (few rows, memory-bound): quantize + GEMM from fp16 x.
+
+    Weight copies are rotated past the 256 MB Infinity Cache.  Algorithmic bytes of
+    the GEMM: M K/2 + N K/2 + 2 (M + N) K/G + 2 M N; the linear adds the fp16 x
+    (2 M K).  Also times the fp16 GEMM of the same shape (torch -> hipBLASLt).
+    """
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    out = []
+    wcache = {}
+    for (Md, Nd, Kd) in DECODE_CASES:
+        Gd = 128
+        if (Nd, Kd) not in wcache:
+            w = torch.from_numpy(wl.weights(wl.rng_for("decode", 2, Nd), Nd, Kd)).to(dev)
+            Wq, sw = pk.apex4_quantize_act(w, Gd)
+            Rw = max(2, -(-ROTATE_BYTES // (Nd * Kd // 2 + 2 * Nd * (Kd // Gd))))
+            Rf = max(2, -(-ROTATE_BYTES // (2 * Nd * Kd)))
+            wcache.clear()
+            wcache[(Nd, Kd)] = ([(Wq.clone(), sw.clone()) for _ in range(Rw)], [w.clone() for _ in range(Rf)])
+            del w, Wq, sw
+        qsets, fsets = wcache[(Nd, Kd)]
+        x = torch.from_numpy(wl.activations(wl.rng_for("decode", 1, Md * 1000 + Nd // 1024), Md, Kd)).to(dev)
+        Aq = torch.empty((Md, Kd // 2), dtype=torch.uint8, device=dev)
+        sa = torch.empty((Md, Kd // Gd), dtype=torch.float16, device=dev)
+        Y = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
+        pk.apex4_quantize_act(x, Gd, Aq, sa)
+
+        def timed(fn):
+            for i in range(5):
+                fn(i)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for i in range(reps):
+                fn(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps * 1e3
+
+        lin_us = timed(lambda i: pk.apex4_w4a4_linear(x, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y, Aq, sa))
+        gemm_us = timed(lambda i: pk.apex4_w4a4_gemm(Aq, sa, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y))
+        yf = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
+        fp16_us = timed(lambda i: torch.matmul(x, fsets[i % len(fsets)].t(), out=yf))
+        gbytes = Md * Kd / 2 + Nd * Kd / 2 + 2 * (Md + Nd) * Kd / Gd + 2 * Md * Nd
+        out.append({"M": Md, "N": Nd, "K": Kd, "G": Gd, "linear_us": round(lin_us, 2), "gemm_us": round(gemm_us, 2),
+                    "gemm_hbm_gbs": round(gbytes / (gemm_us * 1e-6) / 1e9, 1),
+                    "gemm_hbm_frac": round(gbytes / (gemm_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
+                    "linear_hbm_gbs": round((gbytes + 2 * Md * Kd) / (lin_us * 1e-6) / 1e9, 1),
+                    "fp16_gemm_us": round(fp16_us, 2), "speedup_linear_vs_fp16": round(fp16_us / lin_us, 3)})
+        del x, Aq, sa, Y, yf
+    wcache.clear()
+    torch.cuda.synchronize()
+    return out
+
+
 def main():
     args = parse()
     if args.mode == "counters":
@@ -332,6 +395,8 @@ def main():
         "speedup_gemm_vs_fp16": round(fp16_ms / gemm_ms, 3),
         "speedup_step_vs_fp16": round(fp16_ms / ms_per_step, 3),
     }
+    if not args.no_decode:
+        line["decode"] = decode_bench()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(line), flush=True)

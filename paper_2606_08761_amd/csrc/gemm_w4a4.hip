@@ -391,7 +391,8 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
 
 }  // namespace
 
-// Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.
+// Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  Up to 32
+// rows (decode) go to the streaming kernel instead, except for the debug dump.
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P,
                        hipStream_t stream) {
@@ -399,6 +400,7 @@ hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
         if (G <= 256) return launch<1, 8, 4, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         return launch<1, 8, 4, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     }
+    if (decode_fits(M, N, K, G)) return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
     if (G == K) return launch<1, 8, 4, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 128) return launch<1, 8, 4, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 256) return launch<1, 8, 4, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);

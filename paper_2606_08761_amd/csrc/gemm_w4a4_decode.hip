@@ -1,0 +1,214 @@
+// W4A4 group GEMM for few rows (M <= 32: decode and small batches) on gfx950.
+//
+// Same result as the tiled kernel (APEX4 Sec. 3.2.1, Eq. group_decomposition),
+// organised for the memory-bound regime, where the weights are streamed from HBM
+// once and the HBM queue is kept full.
+//   * Work unit: 32 output columns ("tile") by every row.  Workgroups are
+//     persistent (at most one per CU) and walk the tiles blockIdx.x,
+//     blockIdx.x + gridDim.x, ...  Their 8 waves split the 128-wide K stages
+//     round-robin (wave w takes stages w, w + 8, ...), so neighbouring waves read
+//     neighbouring 64-byte runs of every weight row.
+//   * Each wave streams (tile, stage) pairs through a ring of PF stages of packed
+//     weights, activations and weight scales held in registers.  The ring runs
+//     across tile boundaries, so the next tile's loads are in flight while a tile
+//     is reduced and stored.  Every wave walks the same number of stages per
+//     tile: stages past K are re-reads of the last one with weight 0, which
+//     keeps the per-tile barriers uniform.
+//   * Per stage, four v_mfma_i32_32x32x32_i8 with the activations as the first
+//     operand (lane l holds output column l % 32 and 16 rows) give exactly
+//     256 x the stage's partial group sum.  The partial is dequantized right away
+//     with its group's scales.  Dequantization is linear in P, so splitting a
+//     group into 128-wide partials changes only the fp32 rounding, never the
+//     exact group sum.  Every partial satisfies |256 P| <= 2^21, so the
+//     1.5 * 2^23 accumulator bias gives the float conversion for free at every G.
+//     The weight scale is one value per lane.  The activation scales of all rows
+//     and groups (at most 32 * K/G binary16) sit in LDS for the whole kernel.
+//   * The 8 partial fp32 tiles are summed through LDS in a fixed order and
+//     rounded once to binary16.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "apex4_internal.h"
+
+namespace apex4 {
+namespace {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int NWAVE = 8;
+constexpr int COLS = 32;
+constexpr int ROWS = 32;
+constexpr int PF = 4;                          // stages in flight per wave
+constexpr int MAX_SA_LDS = 64 * 1024;         // bytes of staged activation scales
+constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
+constexpr float MAGIC = 12582912.0f;
+
+__device__ __forceinline__ float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+__device__ __forceinline__ uint32_t even_w(uint32_t w) { return (w << 4) & 0xF0F0F0F0u; }
+__device__ __forceinline__ uint32_t odd_w(uint32_t w) { return w & 0xF0F0F0F0u; }
+__device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
+    i32x4 r;
+    r[0] = static_cast<int>(even_w(w0));
+    r[1] = static_cast<int>(odd_w(w0));
+    r[2] = static_cast<int>(even_w(w1));
+    r[3] = static_cast<int>(odd_w(w1));
+    return r;
+}
+
+__global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
+    const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
+    const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
+    __shared__ float red[NWAVE][16][64];
+    extern __shared__ uint16_t sas[];  // [K/G][32]: activation scale of row r, group g at g * 32 + r
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int nks = K / 128;
+    const int ng = K / G;
+    const int spg = G / 128;
+    const int ntiles = (N + COLS - 1) / COLS;
+    const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
+    const int per_tile = (nks + NWAVE - 1) / NWAVE;  // stages per wave per tile (the last may be null)
+    const int total = my_tiles * per_tile;
+
+    // activation scales; rows past M are clamped (their outputs are never stored)
+    for (int i = tid; i < ng * ROWS; i += 64 * NWAVE) {
+        const int r = i / ng, g = i - r * ng;
+        sas[g * ROWS + r] = sa[static_cast<int64_t>(min(r, M - 1)) * ng + g];
+    }
+
+    const uint8_t* arow = Aq + static_cast<int64_t>(min(l32, M - 1)) * (K / 2) + 32 * lh;
+
+    // ring of in-flight stages
+    uint4 rw[PF][2], ra[PF][2];
+    uint32_t rs[PF];
+    auto load = [&](int j, int q) {
+        q = min(q, total - 1);
+        const int t = q / per_tile, i = q - t * per_tile;
+        const int s = min(wave + NWAVE * i, nks - 1);
+        const int n = min((blockIdx.x + t * gridDim.x) * COLS + l32, N - 1);
+        const uint8_t* wrow = Wq + static_cast<int64_t>(n) * (K / 2) + 32 * lh + s * 64;
+        rw[j][0] = *reinterpret_cast<const uint4*>(wrow);
+        rw[j][1] = *reinterpret_cast<const uint4*>(wrow + 16);
+        ra[j][0] = *reinterpret_cast<const uint4*>(arow + s * 64);
+        ra[j][1] = *reinterpret_cast<const uint4*>(arow + s * 64 + 16);
+        rs[j] = sw[static_cast<int64_t>(n) * ng + s / spg];
+    };
+
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    i32x16 start;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) start[r] = static_cast<int>(MAGIC_BITS);
+
+    if (total > 0) {
+#pragma unroll
+        for (int j = 0; j < PF; ++j) load(j, j);
+    }
+    __syncthreads();  // activation scales staged
+
+    auto process = [&](int j, int q) {
+        const int t = q / per_tile, i = q - t * per_tile;
+        const int s_raw = wave + NWAVE * i;
+        const bool live = s_raw < nks;
+        const int g = min(s_raw, nks - 1) / spg;
+        i32x4 bw[4], af[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const uint4& v = rw[j][kk >> 1];
+            const uint4& u = ra[j][kk >> 1];
+            bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
+            af[kk] = (kk & 1) ? frag2(u.z, u.w) : frag2(u.x, u.y);
+        }
+        i32x16 d = start;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk], bw[kk], d, 0, 0, 0);
+        const float s1 = live ? h2f(static_cast<uint16_t>(rs[j])) * (1.0f / 256.0f) : 0.f;
+        const float nb = -MAGIC * s1;
+        uint2 sah[4];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t pair = (r & 2) ? sah[r >> 2].y : sah[r >> 2].x;
+            const uint16_t h = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
+            const float tt = fmaf(__int_as_float(d[r]), s1, nb);
+            acc[r] = fmaf(tt, h2f(h), acc[r]);
+        }
+    };
+
+    // reduce the 8 partial tiles of tile t, store, and clear the accumulator
+    auto finish_tile = [&](int t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[wave][r][lane] = acc[r];
+        __syncthreads();
+        const int n0 = (blockIdx.x + t * gridDim.x) * COLS;
+        for (int o = tid; o < 16 * 64; o += 64 * NWAVE) {
+            const int r = o >> 6, ln = o & 63;
+            float v = 0.f;
+#pragma unroll
+            for (int w = 0; w < NWAVE; ++w) v += red[w][r][ln];
+            const int row = 8 * (r >> 2) + 4 * (ln >> 5) + (r & 3);
+            const int col = n0 + (ln & 31);
+            if (row < M && col < N) Y[static_cast<int64_t>(row) * N + col] = __half_as_ushort(__float2half_rn(v));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    };
+
+    for (int q0 = 0; q0 < total; q0 += PF) {
+#pragma unroll
+        for (int j = 0; j < PF; ++j) {
+            const int q = q0 + j;
+            if (q < total) {  // uniform across the workgroup
+                process(j, q);
+                load(j, q + PF);
+                if ((q + 1) % per_tile == 0) finish_tile(q / per_tile);
+            }
+        }
+    }
+}
+
+int cu_count() {
+    static int n = 0;  // benign race: every caller computes the same value
+    if (n == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            n = v;
+        else
+            return 256;
+    }
+    return n;
+}
+
+}  // namespace
+
+bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+    return M >= 1 && M <= ROWS && N >= 1 && (K / G) * ROWS * 2 <= MAX_SA_LDS;
+}
+
+hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
+                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+    if (!decode_fits(M, N, K, G)) return hipErrorInvalidValue;
+    static bool lds_attr_set = false;  // benign race: every caller sets the same value
+    if (!lds_attr_set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(w4a4_decode_kernel),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, MAX_SA_LDS);
+        if (e != hipSuccess) return e;
+        lds_attr_set = true;
+    }
+    const int64_t tiles = (N + COLS - 1) / COLS;
+    const int64_t grid = tiles < cu_count() ? tiles : cu_count();
+    const size_t lds = static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
+    hipLaunchKernelGGL(w4a4_decode_kernel, dim3(static_cast<unsigned>(grid)), dim3(64 * NWAVE), lds, stream, Aq, sa,
+                       Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y);
+    return hipGetLastError();
+}
+
+}  // namespace apex4

@@ -162,6 +162,44 @@ def test_decode_linear(O, N, K):
         assert torch.equal(Y, Y2)
 
 
+DECODE = [
+    (1, 96, 4224, 128), (5, 40, 2560, 512), (32, 300, 1536, 1536), (16, 64, 28672, 256),
+    (3, 1000, 1152, 128), (31, 33, 640, 128), (32, 8192, 8192, 512),
+]
+
+
+@pytest.mark.parametrize("M,N,K,G", DECODE)
+def test_decode_kernel_shapes(O, M, N, K, G):
+    """Up to 32 rows run on the weight-streaming kernel (K split over 8 waves)."""
+    log(f"decode kernel M={M} N={N} K={K} G={G}")
+    r = np.random.default_rng(M * 104729 + N * 13 + K + G)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+    check_tolerance(run_gemm(Aq, sa, Wq, sw, G), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"decode {M}x{N}x{K} G{G}")
+
+
+@pytest.mark.parametrize("G", [128, 512])
+def test_decode_extreme_codes(O, G):
+    M, N, K = 8, 72, 2048
+    Aq = np.full((M, K // 2), 0x88, np.uint8)
+    Wq = np.full((N, K // 2), 0x88, np.uint8)
+    Wq[::2] = 0x77
+    s_a = np.full((M, K // G), 2.0 ** -7, np.float16)
+    s_w = np.full((N, K // G), 2.0 ** -7, np.float16)
+    check_tolerance(run_gemm(Aq, s_a, Wq, s_w, G), O.gemm_rows(Aq, s_a, Wq, s_w, K, G), "decode extreme")
+
+
+def test_decode_repeatable():
+    import torch
+    m = pk()
+    M, N, K, G = 16, 520, 3072, 128
+    Aq, sa, Wq, sw = wl.codes_workload("tiny", M, N, K, G)
+    a, s1, w, s2 = dev(Aq), dev(sa), dev(Wq), dev(sw)
+    Y1 = m.apex4_w4a4_gemm(a, s1, w, s2, G)
+    for _ in range(5):
+        assert torch.equal(m.apex4_w4a4_gemm(a, s1, w, s2, G), Y1)
+
+
 def test_repeatable_and_degenerate():
     import torch
     m = pk()
