@@ -102,3 +102,39 @@ def test_deterministic_and_m_zero():
     assert torch.equal(q1, q2) and torch.equal(s1, s2)
     # M == 0 is a successful no-op
     pk.apex4_quantize_act(torch.empty((0, 2048), dtype=torch.float16, device="cuda"), 128)
+
+
+def _every_value_groups(G: int, amax_bits: list[int]) -> np.ndarray:
+    """Rows of groups whose amax is fixed (first element) and whose other
+    elements run through every binary16 value of magnitude <= amax, both signs."""
+    rows = []
+    for ab in amax_bits:
+        mags = np.arange(0, ab + 1, dtype=np.uint16)                      # every magnitude <= amax
+        vals = np.concatenate([mags, mags | np.uint16(0x8000)])            # both signs
+        per = G - 1
+        n = -(-len(vals) // per)
+        body = np.zeros(n * per, np.uint16)
+        body[:len(vals)] = vals
+        groups = np.concatenate([np.full((n, 1), ab, np.uint16), body.reshape(n, per)], axis=1)
+        rows.append(groups.reshape(-1))
+    flat = np.concatenate(rows)
+    K = 8 * G
+    pad = (-len(flat)) % K
+    flat = np.concatenate([flat, np.zeros(pad, np.uint16)])
+    return flat.reshape(-1, K).view(np.float16)
+
+
+# amax bit patterns: subnormal scales (clamp at -8 and +7 fires), exact powers of
+# two times 7 (many exact ties), and ordinary values
+AMAX_BITS = [0x0001, 0x0003, 0x0004, 0x000A, 0x000D, 0x0031, 0x00E0, 0x03FF, 0x0400, 0x1F00, 0x2700,
+             0x2B00, 0x3300, 0x3700, 0x3B00, 0x4700, 0x3C00, 0x4000, 0x4200, 0x4488, 0x4BFF, 0x5555,
+             0x5F00, 0x6300, 0x6B00, 0x7700, 0x7BFF]
+
+
+@pytest.mark.parametrize("G", [32, 128, 512, 1024])
+def test_every_binary16_value(O, G):
+    """Every binary16 magnitude <= amax, for 27 group maxima, bit-exact against the oracle."""
+    bits = AMAX_BITS if G == 128 else AMAX_BITS[::3]
+    x = _every_value_groups(G, bits)
+    log(f"quantize every binary16 value G={G} ({x.shape[0]} x {x.shape[1]})")
+    assert_same(x, G, O, f"every value G={G}")
