@@ -17,6 +17,7 @@ MFMA_32x32x32_I8_OPS = 2 * 32 * 32 * 32
 MFMA_16x16x64_I8_OPS = 2 * 16 * 16 * 64
 WAVE = 64
 INTERLEAVE_V = (0, 2, 4, 6, 7, 8, 12)
+INTERLEAVE_V_2W = (0, 2, 4, 6, 8, 11, 16)
 
 
 def rho_from_table(int_tops: float, fp32_tflops: float) -> float:
@@ -34,6 +35,8 @@ def _lib():
     L.apex4_copy_probe.restype = ctypes.c_int
     L.apex4_rho_probe_ext.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int]
     L.apex4_rho_probe_ext.restype = ctypes.c_int
+    L.apex4_rho_probe_issue.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int]
+    L.apex4_rho_probe_issue.restype = ctypes.c_int
     return L
 
 
@@ -57,8 +60,13 @@ def measure() -> dict:
         raise RuntimeError(f"apex4_rho_probe failed: {rc}")
     o = list(out)
     mfma_ops_clk_simd = MFMA_32x32x32_I8_OPS / o[0]
-    fma_flops_clk_simd = 2 * WAVE / o[2]            # one FMA = 2 flops per lane
+    fma_flops_clk_simd = 2 * WAVE / o[2]            # one FMA = 2 flops per lane (one wave per SIMD)
     cvt_ops_clk_simd = 2 * WAVE / o[3]              # two converts per measured pair
+    iss = (ctypes.c_double * 9)()
+    if L.apex4_rho_probe_issue(iss, 9) != 0:
+        raise RuntimeError("apex4_rho_probe_issue failed")
+    i9 = list(iss)
+    fma_sustained_clk_simd = 2 * WAVE / min(i9[0], i9[1])   # several waves per SIMD
     res = {
         "cycles_per_mfma_i32_32x32x32_i8": o[0],
         "cycles_per_mfma_i32_16x16x64_i8": o[1],
@@ -68,7 +76,12 @@ def measure() -> dict:
         "int8_mfma16_ops_per_clk_per_cu": 4 * MFMA_16x16x64_I8_OPS / o[1],
         "fp32_fma_flops_per_clk_per_cu": 4 * fma_flops_clk_simd,
         "cvt_ops_per_clk_per_cu": 4 * cvt_ops_clk_simd,
-        "rho_measured": mfma_ops_clk_simd / fma_flops_clk_simd,
+        "rho_measured": mfma_ops_clk_simd / fma_sustained_clk_simd,
+        "rho_measured_one_wave_per_simd": mfma_ops_clk_simd / fma_flops_clk_simd,
+        "cycles_per_v_fma_f32_per_simd_2_waves": i9[0],
+        "cycles_per_v_fma_f32_per_simd_4_waves": i9[1],
+        "fp32_fma_flops_per_clk_per_cu_sustained": 4 * fma_sustained_clk_simd,
+        "mfma_cycles_per_simd_2_waves_v_fma_interleaved": {str(v): i9[2 + i] for i, v in enumerate(INTERLEAVE_V_2W)},
         "rho_datasheet_packed_fp32": rho_from_table(5033.2, 157.3),
         "rho_datasheet_unpacked_fp32": rho_from_table(5033.2, 78.6),
         "mfma_cycles_with_v_fma_interleaved": {str(v): o[4 + i] for i, v in enumerate(INTERLEAVE_V)},

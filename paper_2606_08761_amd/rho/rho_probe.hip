@@ -23,8 +23,8 @@ __device__ __forceinline__ uint64_t rt100() { return __builtin_amdgcn_s_memrealt
 
 // v_mfma_i32_32x32x32_i8, 4 independent accumulator chains; `vfma` independent
 // v_fma_f32 per MFMA interleaved in the same wave.
-template <int VFMA>
-__global__ __launch_bounds__(256) void mfma32_kernel(int seed, uint64_t* cycles, int* sink) {
+template <int VFMA, int NT = 256>
+__global__ __launch_bounds__(NT) void mfma32_kernel(int seed, uint64_t* cycles, int* sink) {
     i32x4 a = {seed, seed + 1, seed + 2, seed + 3};
     i32x4 b = {seed * 3, seed ^ 5, seed + 7, seed - 1};
     i32x16 acc0 = {}, acc1 = {}, acc2 = {}, acc3 = {};
@@ -71,8 +71,8 @@ __global__ __launch_bounds__(256) void mfma32_kernel(int seed, uint64_t* cycles,
     int s = 0;
 #pragma unroll
     for (int i = 0; i < 16; ++i) s += acc0[i] + acc1[i] + acc2[i] + acc3[i] + static_cast<int>(f[i]);
-    if (s == 0x7fffffff) sink[threadIdx.x] = s;
-    if ((threadIdx.x & 63) == 0) cycles[blockIdx.x * 4 + (threadIdx.x >> 6)] = t1 - t0;
+    if (s == 0x7fffffff) sink[threadIdx.x & 255] = s;
+    if ((threadIdx.x & 63) == 0) cycles[blockIdx.x * (NT / 64) + (threadIdx.x >> 6)] = t1 - t0;
 }
 
 __global__ __launch_bounds__(256) void mfma16_kernel(int seed, uint64_t* cycles, int* sink) {
@@ -93,11 +93,13 @@ __global__ __launch_bounds__(256) void mfma16_kernel(int seed, uint64_t* cycles,
 }
 
 // 16 independent chains of v_fma_f32 (per iteration 16 instructions).
-__global__ __launch_bounds__(256) void fma_kernel(int seed, uint64_t* cycles, int* sink) {
+template <int NT = 256>
+__global__ __launch_bounds__(NT) void fma_kernel(int seed, uint64_t* cycles, int* sink) {
     float f[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) f[i] = seed * 0.5f + i;
     const float m = 1.0001f, c = 0.5f;
+    __builtin_amdgcn_s_barrier();
     const uint64_t t0 = cyc();
     for (int it = 0; it < ITERS; ++it) {
 #pragma unroll
@@ -107,8 +109,8 @@ __global__ __launch_bounds__(256) void fma_kernel(int seed, uint64_t* cycles, in
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) s += f[i];
-    if (s == 1234.5f) sink[threadIdx.x] = 1;
-    if ((threadIdx.x & 63) == 0) cycles[blockIdx.x * 4 + (threadIdx.x >> 6)] = t1 - t0;
+    if (s == 1234.5f) sink[threadIdx.x & 255] = 1;
+    if ((threadIdx.x & 63) == 0) cycles[blockIdx.x * (NT / 64) + (threadIdx.x >> 6)] = t1 - t0;
 }
 
 // 16 independent v_cvt_f32_i32 + v_cvt_i32_f32 pairs per iteration (32 instructions).
@@ -305,7 +307,7 @@ extern "C" int apex4_rho_probe(double* out, int n_out) {
     };
     out[0] = run4(mfma32_kernel<0>, ITERS * 4.0);
     out[1] = run4(mfma16_kernel, ITERS * 8.0);
-    out[2] = run4(fma_kernel, ITERS * 16.0);
+    out[2] = run4(fma_kernel<256>, ITERS * 16.0);
     out[3] = run4(cvt_kernel, ITERS * 16.0);
     out[4] = run4(mfma32_kernel<0>, ITERS * 4.0);
     out[5] = run4(mfma32_kernel<2>, ITERS * 4.0);
@@ -338,6 +340,58 @@ extern "C" int apex4_rho_probe(double* out, int n_out) {
         out[14] = h[2] ? 100.0 * static_cast<double>(h[1]) / static_cast<double>(h[2]) : 0;
     }
     out[15] = ncu;
+    delete[] h;
+    (void)hipFree(cyc_d);
+    (void)hipFree(sink);
+    return rc;
+}
+
+// Sustained issue rates with several waves per SIMD (cycles per SIMD):
+//   out[0] cycles per v_fma_f32 with 2 waves per SIMD
+//   out[1] cycles per v_fma_f32 with 4 waves per SIMD
+//   out[2 + i], i = 0..6: cycles per v_mfma_i32_32x32x32_i8 with 2 waves per
+//          SIMD, each wave interleaving V = {0, 2, 4, 6, 8, 11, 16} independent
+//          v_fma_f32 per MFMA
+extern "C" int apex4_rho_probe_issue(double* out, int n_out) {
+    if (!out || n_out < 9) return -1;
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return -2;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -2;
+    uint64_t* cyc_d = nullptr;
+    int* sink = nullptr;
+    const int nw = ncu * 16;
+    if (hipMalloc(&cyc_d, sizeof(uint64_t) * nw) != hipSuccess) return -3;
+    if (hipMalloc(&sink, sizeof(int) * 256) != hipSuccess) { (void)hipFree(cyc_d); return -3; }
+    uint64_t* h = new uint64_t[nw];
+    const size_t hold = 96 * 1024;
+    int rc = 0;
+    // Per-SIMD cycles per instruction: the waves of a workgroup start together
+    // (barrier), so the slowest wave's count is the elapsed time of its SIMD;
+    // divide by the instructions all waves of that SIMD issued.
+    auto run = [&](void (*k)(int, uint64_t*, int*), int threads, double per_wave) -> double {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  static_cast<int>(hold));
+        hipLaunchKernelGGL(k, dim3(ncu), dim3(threads), hold, 0, 3, cyc_d, sink);
+        if (hipDeviceSynchronize() != hipSuccess) { rc = -4; return 0; }
+        const int waves = threads / 64;
+        (void)hipMemcpy(h, cyc_d, sizeof(uint64_t) * ncu * waves, hipMemcpyDeviceToHost);
+        double sum = 0;
+        for (int b = 0; b < ncu; ++b) {
+            uint64_t mx = 0;
+            for (int w = 0; w < waves; ++w) mx = h[b * waves + w] > mx ? h[b * waves + w] : mx;
+            sum += static_cast<double>(mx);
+        }
+        return sum / ncu / (per_wave * (waves / 4));
+    };
+    out[0] = run(fma_kernel<512>, 512, ITERS * 16.0);
+    out[1] = run(fma_kernel<1024>, 1024, ITERS * 16.0);
+    out[2] = run(mfma32_kernel<0, 512>, 512, ITERS * 4.0);
+    out[3] = run(mfma32_kernel<2, 512>, 512, ITERS * 4.0);
+    out[4] = run(mfma32_kernel<4, 512>, 512, ITERS * 4.0);
+    out[5] = run(mfma32_kernel<6, 512>, 512, ITERS * 4.0);
+    out[6] = run(mfma32_kernel<8, 512>, 512, ITERS * 4.0);
+    out[7] = run(mfma32_kernel<11, 512>, 512, ITERS * 4.0);
+    out[8] = run(mfma32_kernel<16, 512>, 512, ITERS * 4.0);
     delete[] h;
     (void)hipFree(cyc_d);
     (void)hipFree(sink);
