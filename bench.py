@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize"), default="bench",
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep"), default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
                         "summarize: turn rocprofv3 CSV output into the profiles/ summaries")
@@ -55,6 +55,9 @@ def parse():
     p.add_argument("--write-csv", help="summarize: counter_collection.csv of the WRITE_SIZE pass")
     p.add_argument("--stats-csv", help="summarize: kernel_stats.csv of the --kernel-trace --stats run")
     p.add_argument("--commands", help="summarize: text file with the exact commands that made the CSVs")
+    p.add_argument("--bench-log", help="summarize: output of the traced bench run (its JSON line)")
+    p.add_argument("--gsweep-trace", help="summarize: kernel_stats.csv of the --kernel-trace --stats run of --mode gsweep")
+    p.add_argument("--gsweep-pmc", help="summarize: counter_collection.csv of the SQ counter pass over --mode gsweep")
     return p.parse_args()
 
 
@@ -154,7 +157,7 @@ def summarize_mode(args):
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
              "## Kernel trace (`--kernel-trace --stats`, bench.py default workload)", "",
              "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
-    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:8]:
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:12]:
         name = r["Name"]
         m = re.search(r"(\w+_kernel(?:<[^()]*>)?)", name)
         short = (m.group(1) if m else name.split("(")[0])[:80]
@@ -168,9 +171,77 @@ def summarize_mode(args):
               f"* algorithmic bytes per launch: {alg / 1e6:.1f} MB; measured / algorithmic = "
               f"{(read_b + write_b) / alg:.2f}",
               f"* kernel source sha256: `{prof['kernel_source_sha256']}`"]
+    if args.bench_log:
+        line = [l for l in open(args.bench_log) if l.startswith("{")][-1]
+        b = json.loads(line)
+        lines += ["", "## Per-workload timing of the traced bench run (HIP events in bench.py, same process)", "",
+                  f"* quantizer, x[{M},{K}] G={G}: {b['quant_us']:.1f} us ({b['quant_hbm_gbs']:.0f} GB/s of "
+                  f"{2.5 * M * K + 2 * M * K / G:.3g} algorithmic bytes)",
+                  f"* W4A4 GEMM {M}x{N}x{K} G={G}: {b['gemm_us']:.1f} us ({b['gemm_tops']:.0f} TOPS); "
+                  f"fp16 GEMM (hipBLASLt) {b['fp16_gemm_us']:.1f} us",
+                  "", "| decode M | N | K | quantize + GEMM us | GEMM us | GEMM HBM GB/s | fp16 GEMM us | speedup vs fp16 |",
+                  "|---|---|---|---|---|---|---|---|"]
+        for d in b.get("decode", []):
+            lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d['linear_us']} | {d['gemm_us']} | {d['gemm_hbm_gbs']} | "
+                         f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} |")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
+    if args.gsweep_trace and args.gsweep_pmc:
+        summarize_gsweep(args.gsweep_trace, args.gsweep_pmc, cmds)
     print(json.dumps(prof, indent=1))
+
+
+GSWEEP_MODES = {"0, true": 128, "1, true": 256, "1, false": 512, "2, false": 8192}
+
+
+def summarize_gsweep(trace_csv, pmc_csv, cmds):
+    """profiles/gemm_w4a4_gsweep_m4096.md: per group size, kernel time and the
+    VALU / MFMA instruction counts per wave and group (SQ counters)."""
+    import csv
+    import statistics
+    Mg, Ng, Kg, _ = GSWEEP
+    waves = -(-Mg // 128) * -(-Ng // 256) * 8
+
+    def mode_of(name):
+        m = re.search(r"w4a4_gemm_kernel<1, 8, 4, 1, (\d, (?:true|false))>", name)
+        return GSWEEP_MODES.get(m.group(1)) if m else None
+
+    times = {}
+    for r in csv.DictReader(open(trace_csv)):
+        g = mode_of(r["Name"])
+        if g:
+            times[g] = float(r["AverageNs"]) / 1e3
+    cnt = {}
+    for r in csv.DictReader(open(pmc_csv)):
+        g = mode_of(r["Kernel_Name"])
+        if g:
+            cnt.setdefault(g, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    c = {g: {k: statistics.mean(v) for k, v in d.items()} for g, d in cnt.items()}
+    base_valu = c[Kg]["SQ_INSTS_VALU"]
+    lines = [f"# W4A4 GEMM granularity sweep, M={Mg} N=K={Ng}: rocprofv3 summary", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
+             "Per group and wave (one wave owns 128 x 32 outputs): MFMA cycles = MFMAs x 32 (v_mfma_i32_32x32x32_i8); "
+             "dequant VALU cycles = (VALU instructions - those at G=K) x 4 (one wave64 VALU instruction per 4 SIMD cycles, "
+             "measured). TOPS = 2MNK / average kernel time (kernel trace).", "",
+             "| G | kernel us | TOPS | % INT8 peak | VALU/MFMA (instructions) | MFMA/wave/group | dequant VALU/wave/group "
+             "| MFMA cycles/group | dequant VALU cycles/group | VALU/MFMA cycles |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for g in sorted(c):
+        groups = Kg // g
+        mf = c[g]["SQ_INSTS_MFMA"] / waves / groups
+        dq = (c[g]["SQ_INSTS_VALU"] - base_valu) / waves / groups if g != Kg else 0.0
+        t = times.get(g)
+        tops = 2.0 * Mg * Ng * Kg / t / 1e6 if t else float("nan")
+        lines.append(f"| {g} | {t:.1f} | {tops:.0f} | {100 * tops / INT8_PEAK_TOPS:.1f} | "
+                     f"{c[g]['SQ_INSTS_VALU'] / c[g]['SQ_INSTS_MFMA']:.2f} | {mf:.0f} | {dq:.1f} | {mf * 32:.0f} | "
+                     f"{dq * 4:.0f} | {dq * 4 / (mf * 32):.2f} |")
+    lines += ["", "Raw SQ counters per dispatch (means):", "",
+              "| G | " + " | ".join(sorted(next(iter(c.values())))) + " |",
+              "|---|" + "---|" * len(next(iter(c.values())))]
+    for g in sorted(c):
+        lines.append(f"| {g} | " + " | ".join(f"{c[g][k]:.4g}" for k in sorted(c[g])) + " |")
+    with open(os.path.join(ROOT, "profiles", "gemm_w4a4_gsweep_m4096.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def counters_mode():
@@ -192,6 +263,37 @@ def counters_mode():
     torch.cuda.synchronize()
     print(json.dumps({"mode": "counters", "copy_bytes": 256 << 20, "gemm": [M, N, K, G],
                       "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
+
+
+GSWEEP = (4096, 8192, 8192, (128, 256, 512, 8192))
+
+
+def gsweep_mode(reps: int = 20):
+    """Granularity sweep (the paper's rho-aware group-size choice): M=4096,
+    N=K=8192, G in {128, 256, 512, K}, random codes and scales.  Each G runs its
+    own kernel mode, so per-kernel counters separate by kernel name."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    Mg, Ng, Kg, Gs = GSWEEP
+    stream = torch.cuda.current_stream(dev)
+    for Gg in Gs:
+        c = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("gsweep", Mg, Ng, Kg, Gg)]
+        Y = torch.empty((Mg, Ng), dtype=torch.float16, device=dev)
+        for _ in range(3):
+            pk.apex4_w4a4_gemm(*c, Gg, Y)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            pk.apex4_w4a4_gemm(*c, Gg, Y)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        print(json.dumps({"mode": "gsweep", "M": Mg, "N": Ng, "K": Kg, "G": Gg, "us": round(us, 2),
+                          "tops": round(2.0 * Mg * Ng * Kg / us / 1e6, 1), "launches": reps + 3}), flush=True)
+        del c, Y
 
 
 DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)]
@@ -262,6 +364,8 @@ def main():
         return counters_mode()
     if args.mode == "summarize":
         return summarize_mode(args)
+    if args.mode == "gsweep":
+        return gsweep_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
