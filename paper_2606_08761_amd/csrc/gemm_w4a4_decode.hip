@@ -40,8 +40,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int NWAVE = 8;
 constexpr int COLS = 32;
 constexpr int ROWS = 32;
-constexpr int PF = 4;                          // stages in flight per wave
 constexpr int MAX_SA_LDS = 64 * 1024;         // bytes of staged activation scales
+constexpr int DECODE_PF = 6;                   // stages in flight per wave
 constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
 constexpr float MAGIC = 12582912.0f;
 
@@ -57,10 +57,15 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
     return r;
 }
 
+// MROWS in {8, 16, 32}: the rows that can hold outputs (M <= MROWS); only they
+// are dequantized and reduced.  PF: stages in flight per wave.  Lane l holds rows 8 (r / 4) + 4 (l / 32) + r % 4
+// for r < MROWS / 2.
+template <int MROWS, int PF>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
-    __shared__ float red[NWAVE][16][64];
+    constexpr int NR = MROWS / 2;      // output registers per lane that matter
+    __shared__ float red[NWAVE][NR][64];
     extern __shared__ uint16_t sas[];  // [K/G][32]: activation scale of row r, group g at g * 32 + r
 
     const int tid = threadIdx.x;
@@ -68,9 +73,9 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const int l32 = lane & 31, lh = lane >> 5;
     const int nks = K / 128;
     const int ng = K / G;
-    const int spg = G / 128;
+    const int lg = (G == K) ? 31 : (G == 128 ? 0 : (G == 256 ? 1 : 2));  // group of stage s: s >> lg
     const int ntiles = (N + COLS - 1) / COLS;
-    const int my_tiles = blockIdx.x < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
+    const int my_tiles = static_cast<int>(blockIdx.x) < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
     const int per_tile = (nks + NWAVE - 1) / NWAVE;  // stages per wave per tile (the last may be null)
     const int total = my_tiles * per_tile;
 
@@ -80,42 +85,55 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         sas[g * ROWS + r] = sa[static_cast<int64_t>(min(r, M - 1)) * ng + g];
     }
 
-    const uint8_t* arow = Aq + static_cast<int64_t>(min(l32, M - 1)) * (K / 2) + 32 * lh;
+    // per-lane byte offsets; every load adds a wave-uniform base (stage and group)
+    const uint32_t a_voff = static_cast<uint32_t>(min(l32, M - 1)) * static_cast<uint32_t>(K / 2) + 32 * lh;
+    uint32_t w_voff = 0, s_voff = 0;
+    auto set_tile = [&](int t) {
+        const int n = min((static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS + l32, N - 1);
+        w_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + 32 * lh;
+        s_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(ng);
+    };
 
-    // ring of in-flight stages
+    // ring of in-flight stages; (lt, li) is the next (tile, stage) to load.  No
+    // load is issued past the last stage.
     uint4 rw[PF][2], ra[PF][2];
     uint32_t rs[PF];
-    auto load = [&](int j, int q) {
-        q = min(q, total - 1);
-        const int t = q / per_tile, i = q - t * per_tile;
-        const int s = min(wave + NWAVE * i, nks - 1);
-        const int n = min((blockIdx.x + t * gridDim.x) * COLS + l32, N - 1);
-        const uint8_t* wrow = Wq + static_cast<int64_t>(n) * (K / 2) + 32 * lh + s * 64;
-        rw[j][0] = *reinterpret_cast<const uint4*>(wrow);
-        rw[j][1] = *reinterpret_cast<const uint4*>(wrow + 16);
-        ra[j][0] = *reinterpret_cast<const uint4*>(arow + s * 64);
-        ra[j][1] = *reinterpret_cast<const uint4*>(arow + s * 64 + 16);
-        rs[j] = sw[static_cast<int64_t>(n) * ng + s / spg];
+    int lt = 0, li = 0;
+    auto load = [&](int j) {
+        const int s = min(wave + NWAVE * li, nks - 1);
+        const uint8_t* wb = Wq + static_cast<int64_t>(s) * 64;
+        const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
+        rw[j][0] = *reinterpret_cast<const uint4*>(wb + w_voff);
+        rw[j][1] = *reinterpret_cast<const uint4*>(wb + w_voff + 16);
+        ra[j][0] = *reinterpret_cast<const uint4*>(ab + a_voff);
+        ra[j][1] = *reinterpret_cast<const uint4*>(ab + a_voff + 16);
+        rs[j] = (sw + (s >> lg))[s_voff];
+        if (++li == per_tile) {
+            if (lt + 1 < my_tiles) {
+                li = 0;
+                set_tile(++lt);
+            } else {
+                li = per_tile - 1;
+            }
+        }
     };
 
     f32x16 acc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-    i32x16 start;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) start[r] = static_cast<int>(MAGIC_BITS);
 
     if (total > 0) {
+        set_tile(0);
 #pragma unroll
-        for (int j = 0; j < PF; ++j) load(j, j);
+        for (int j = 0; j < PF; ++j) load(j);
     }
     __syncthreads();  // activation scales staged
 
-    auto process = [&](int j, int q) {
-        const int t = q / per_tile, i = q - t * per_tile;
-        const int s_raw = wave + NWAVE * i;
+    int pi = 0;  // stage-in-tile of the next processed stage
+    auto process = [&](int j) {
+        const int s_raw = wave + NWAVE * pi;
         const bool live = s_raw < nks;
-        const int g = min(s_raw, nks - 1) / spg;
+        const int g = min(s_raw, nks - 1) >> lg;
         i32x4 bw[4], af[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
@@ -124,16 +142,18 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
             bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             af[kk] = (kk & 1) ? frag2(u.z, u.w) : frag2(u.x, u.y);
         }
-        i32x16 d = start;
+        i32x16 d;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) d[r] = static_cast<int>(MAGIC_BITS);
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk], bw[kk], d, 0, 0, 0);
         const float s1 = live ? h2f(static_cast<uint16_t>(rs[j])) * (1.0f / 256.0f) : 0.f;
         const float nb = -MAGIC * s1;
         uint2 sah[4];
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
+        for (int q4 = 0; q4 < NR / 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < NR; ++r) {
             const uint32_t pair = (r & 2) ? sah[r >> 2].y : sah[r >> 2].x;
             const uint16_t h = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
             const float tt = fmaf(__int_as_float(d[r]), s1, nb);
@@ -144,10 +164,10 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     // reduce the 8 partial tiles of tile t, store, and clear the accumulator
     auto finish_tile = [&](int t) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) red[wave][r][lane] = acc[r];
+        for (int r = 0; r < NR; ++r) red[wave][r][lane] = acc[r];
         __syncthreads();
-        const int n0 = (blockIdx.x + t * gridDim.x) * COLS;
-        for (int o = tid; o < 16 * 64; o += 64 * NWAVE) {
+        const int n0 = (static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS;
+        for (int o = tid; o < NR * 64; o += 64 * NWAVE) {
             const int r = o >> 6, ln = o & 63;
             float v = 0.f;
 #pragma unroll
@@ -161,14 +181,17 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         for (int r = 0; r < 16; ++r) acc[r] = 0.f;
     };
 
+    int pt = 0;
     for (int q0 = 0; q0 < total; q0 += PF) {
 #pragma unroll
         for (int j = 0; j < PF; ++j) {
-            const int q = q0 + j;
-            if (q < total) {  // uniform across the workgroup
-                process(j, q);
-                load(j, q + PF);
-                if ((q + 1) % per_tile == 0) finish_tile(q / per_tile);
+            if (q0 + j < total) {  // uniform across the workgroup
+                process(j);
+                if (q0 + j + PF < total) load(j);
+                if (++pi == per_tile) {
+                    finish_tile(pt++);
+                    pi = 0;
+                }
             }
         }
     }
@@ -187,28 +210,41 @@ int cu_count() {
     return n;
 }
 
-}  // namespace
-
-bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
-    return M >= 1 && M <= ROWS && N >= 1 && (K / G) * ROWS * 2 <= MAX_SA_LDS;
-}
-
-hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
-                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
-    if (!decode_fits(M, N, K, G)) return hipErrorInvalidValue;
+template <int PF>
+hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                            int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
     static bool lds_attr_set = false;  // benign race: every caller sets the same value
     if (!lds_attr_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(w4a4_decode_kernel),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, MAX_SA_LDS);
-        if (e != hipSuccess) return e;
+        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF>)}) {
+            const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, MAX_SA_LDS);
+            if (e != hipSuccess) return e;
+        }
         lds_attr_set = true;
     }
     const int64_t tiles = (N + COLS - 1) / COLS;
     const int64_t grid = tiles < cu_count() ? tiles : cu_count();
     const size_t lds = static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
-    hipLaunchKernelGGL(w4a4_decode_kernel, dim3(static_cast<unsigned>(grid)), dim3(64 * NWAVE), lds, stream, Aq, sa,
-                       Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y);
+    const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
+    const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
+    if (M <= 8) hipLaunchKernelGGL((w4a4_decode_kernel<8, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+    else if (M <= 16) hipLaunchKernelGGL((w4a4_decode_kernel<16, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+    else hipLaunchKernelGGL((w4a4_decode_kernel<32, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
     return hipGetLastError();
+}
+
+}  // namespace
+
+bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+    const bool g_ok = G == K || G == 128 || G == 256 || G == 512;
+    return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SA_LDS;
+}
+
+hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
+                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+    if (!decode_fits(M, N, K, G)) return hipErrorInvalidValue;
+    return launch_decode_pf<DECODE_PF>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
 }
 
 }  // namespace apex4
