@@ -17,6 +17,9 @@ hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                        const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
                        uint16_t* Y, int32_t* P, hipStream_t stream);
 
+// Compute units of the current device (cached after the first call).
+int device_cu_count();
+
 // W4A4 GEMM for few rows: weights streamed once, K split over the waves of a
 // workgroup.  decode_fits() says whether the shape is one it handles.
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G);

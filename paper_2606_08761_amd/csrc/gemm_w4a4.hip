@@ -391,20 +391,30 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
 
 }  // namespace
 
-// Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  Up to 32
-// rows (decode) go to the streaming kernel instead, except for the debug dump.
+// Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  When that
+// tiling would not give every CU a workgroup, 64 x 128 tiles with 4 waves of
+// 64 x 32 (four times as many workgroups, two per CU).  Up to 32 rows (decode)
+// go to the streaming kernel instead, except for the debug dump.
+template <int WAVES_N, int MI>
+hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                        int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+    if (P) {
+        if (G <= 256) return launch<1, WAVES_N, MI, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+        return launch<1, WAVES_N, MI, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    }
+    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 128) return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+}
+
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P,
                        hipStream_t stream) {
-    if (P) {
-        if (G <= 256) return launch<1, 8, 4, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-        return launch<1, 8, 4, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    }
-    if (decode_fits(M, N, K, G)) return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
-    if (G == K) return launch<1, 8, 4, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    if (G == 128) return launch<1, 8, 4, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    if (G == 256) return launch<1, 8, 4, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    return launch<1, 8, 4, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (!P && decode_fits(M, N, K, G)) return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
+    const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    if (big_tiles < device_cu_count()) return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
 }
 
 }  // namespace apex4

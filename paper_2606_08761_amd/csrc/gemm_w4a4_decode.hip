@@ -197,19 +197,6 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     }
 }
 
-int cu_count() {
-    static int n = 0;  // benign race: every caller computes the same value
-    if (n == 0) {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-            n = v;
-        else
-            return 256;
-    }
-    return n;
-}
-
 template <int PF>
 hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                             int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
@@ -224,7 +211,7 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
         lds_attr_set = true;
     }
     const int64_t tiles = (N + COLS - 1) / COLS;
-    const int64_t grid = tiles < cu_count() ? tiles : cu_count();
+    const int64_t grid = tiles < device_cu_count() ? tiles : device_cu_count();
     const size_t lds = static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
@@ -235,6 +222,19 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
 }
 
 }  // namespace
+
+int device_cu_count() {
+    static int n = 0;  // benign race: every caller computes the same value
+    if (n == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            n = v;
+        else
+            return 256;
+    }
+    return n;
+}
 
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
     const bool g_ok = G == K || G == 128 || G == 256 || G == 512;
