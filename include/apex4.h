@@ -29,8 +29,9 @@
  * APEX4_ERR_LAUNCH.  Nothing is written when validation fails.
  *
  * Shape rules:  M >= 0, N >= 1, K >= 128 and K % 128 == 0, K % G == 0.
- * Group sizes: the GEMM takes G in {128, 256, 512} or G == K (per-channel,
- * Sec. 3.2.2); the quantizer takes any G with G % 32 == 0 and K % G == 0.
+ * Group sizes: the GEMM takes G in {32, 64, 128, 256, 512, 1024} or G == K
+ * (per-channel); these are the granularities of Sec. 3.2.2 and Sec. 4.1.  The
+ * quantizer takes any G with G % 32 == 0 and K % G == 0.
  * Alignment: every pointer 16-byte aligned.
  * Device: the current device must be gfx950 (MI355X / MI350X).
  */

@@ -42,7 +42,7 @@ int check_gemm_shape(int64_t M, int64_t N, int64_t K) {
 int check_gemm_group(int64_t K, int64_t G) {
     if (G <= 0) return APEX4_ERR_GROUP;
     if (G == K) return APEX4_OK;
-    if (G != 128 && G != 256 && G != 512) return APEX4_ERR_GROUP;
+    if (G != 32 && G != 64 && G != 128 && G != 256 && G != 512 && G != 1024) return APEX4_ERR_GROUP;
     if (K % G != 0) return APEX4_ERR_SHAPE;
     return APEX4_OK;
 }

@@ -36,9 +36,12 @@
 //   * K slots.  In a 128-wide K stage, lane half h of MFMA kk covers
 //     k in [64 h + 16 kk, 64 h + 16 kk + 16): the packed dwords at byte
 //     32 h + 8 kk of the row, widened as even(w0), odd(w0), even(w1), odd(w1).
-//     A lane's weight bytes for a stage are one contiguous 32-byte run.
-//   * Groups.  G == 128: one group per stage, each block's group sum is
-//     dequantized right after its four MFMAs.  G in {256, 512}: group sums
+//     A lane's weight bytes for a stage are one contiguous 32-byte run.  For
+//     G < 128 each MFMA must stay inside one group, so lane half h of MFMA kk
+//     covers k in [32 kk + 16 h, 32 kk + 16 h + 16) (packed byte 16 kk + 8 h).
+//   * Groups.  G in {32, 64}: 4 or 2 whole groups per stage, each dequantized
+//     after its 1 or 2 MFMAs.  G == 128: one group per stage, each block's group
+//     sum is dequantized right after its four MFMAs.  G in {256, 512, 1024}: group sums
 //     persist over the stages of a group.  G == K: sums persist over all of K
 //     and the scales are applied once in the epilogue.
 //   * Workgroup ids are remapped so that each XCD (8 per MI355X, each with its
@@ -64,16 +67,16 @@ constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
 constexpr float MAGIC = 12582912.0f;
 
 enum Mode : int {
-    kRotate = 0,    // G == 128: one group per stage
-    kPersist = 1,   // G in {256, 512}: group sums persist over the stages of a group
+    kRotate = 0,    // G <= 128: whole groups per stage
+    kPersist = 1,   // G in {256, 512, 1024}: group sums persist over the stages of a group
     kChannel = 2,   // G == K: one scale per row and column, applied in the epilogue
     kDump = 3,      // exact integer group sums written out (debug)
 };
 
-template <int BM, int NT>
+template <int BM, int NT, int GPS>
 struct Stage {
     int8_t a[BM * AROW];
-    uint16_t scale[NT];   // [0, BM): s_a rows; [BM, BM + BN): s_w columns; rest unused
+    uint16_t scale[GPS][NT];   // per group of the stage: [0, BM) s_a rows; [BM, BM + BN) s_w columns
 };
 
 __device__ __forceinline__ float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
@@ -90,6 +93,15 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
     return r;
 }
 
+// Compile-time loop: f(integral_constant<int, I>) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 __device__ __forceinline__ i32x16 splat16(int v) {
     i32x16 r;
 #pragma unroll
@@ -99,7 +111,7 @@ __device__ __forceinline__ i32x16 splat16(int v) {
 
 // One workgroup computes a BM x BN tile with WAVES_M x WAVES_N waves; each
 // wave owns MI x NJ blocks of 32 x 32 (rows x columns).
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK>
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
@@ -109,10 +121,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     constexpr int A_CH = BM * 4 / NT;                 // 16-byte packed activation chunks per thread
     constexpr bool ROTATE = MODE == kRotate;
     constexpr bool NEED_ACC = (MODE == kRotate || MODE == kPersist);
+    constexpr bool FINE = GPS > 1;                    // G < 128: GPS whole groups per stage
+    constexpr int KPG = KK / GPS;                     // MFMAs per group and block
     static_assert(A_CH * NT == BM * 4, "tile / thread mismatch");
     static_assert(BM + BN <= NT, "one staged scale per thread");
+    static_assert(!FINE || MODE == kRotate || MODE == kDump, "fine groups rotate or dump");
 
-    __shared__ Stage<BM, NT> st[2];
+    __shared__ Stage<BM, NT, GPS> st[2];
 
     // ---- tile selection (XCD-aware) ----
     const int mt_count = (M + BM - 1) / BM;
@@ -128,7 +143,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, lh = lane >> 5;
     const int nks = K / KS;
-    const int spg = G / KS;           // stages per group
+    const int spg = FINE ? 1 : G / KS;  // stages per group
     const int ng = K / G;
 
     // ---- per-lane offsets (32-bit); uniform stage bases live in scalar registers.
@@ -141,10 +156,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         const int c = tid + i * NT;
         const int r = c >> 2, p = c & 3;
         a_off[i] = static_cast<uint32_t>(min(m0 + r, M - 1)) * static_cast<uint32_t>(K / 2) + p * 16;
-        // packed dwords 4p .. 4p+3 are lane half p/2, MFMAs 2(p%2) and 2(p%2)+1
-        const int c0 = 2 * (2 * (p & 1)) + (p >> 1);
-        a_lds0[i] = r * AROW + c0 * 16;
-        a_lds1[i] = r * AROW + (c0 + 2) * 16;
+        if constexpr (FINE) {
+            // packed bytes 16p .. 16p+7 and 16p+8 .. 16p+15 are MFMA p, lane halves 0 and 1
+            a_lds0[i] = r * AROW + (2 * p) * 16;
+            a_lds1[i] = r * AROW + (2 * p + 1) * 16;
+        } else {
+            // packed dwords 4p .. 4p+3 are lane half p/2, MFMAs 2(p%2) and 2(p%2)+1
+            const int c0 = 2 * (2 * (p & 1)) + (p >> 1);
+            a_lds0[i] = r * AROW + c0 * 16;
+            a_lds1[i] = r * AROW + (c0 + 2) * 16;
+        }
     }
     // Scale staged by this thread: an activation row, a weight column, or (past
     // BM + BN) a clamped dummy that is never read.
@@ -160,16 +181,32 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int n = min(n0 + wn * NJ * 32 + j * 32 + l32, N - 1);
-        w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + 32 * lh;
+        w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + (FINE ? 8 : 32) * lh;
     }
 
     uint4 ra[A_CH];
-    uint16_t rsc = 0;
+    uint16_t rsc[GPS] = {};
     auto load_a = [&](int ks) {
         const uint8_t* base = Aq + static_cast<int64_t>(ks) * (KS / 2);
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
-        if constexpr (MODE != kDump) rsc = (sc_base + ks / spg)[sc_off];
+        if constexpr (MODE != kDump) {
+            // the GPS groups of a stage are adjacent in a scale row (K / G is a multiple of GPS)
+            const uint16_t* sp = sc_base + sc_off + static_cast<uint32_t>(ks / spg) * GPS;
+            if constexpr (GPS == 1) {
+                rsc[0] = *sp;
+            } else if constexpr (GPS == 2) {
+                const uint32_t v = *reinterpret_cast<const uint32_t*>(sp);
+                rsc[0] = static_cast<uint16_t>(v);
+                rsc[1] = static_cast<uint16_t>(v >> 16);
+            } else {
+                const uint2 v = *reinterpret_cast<const uint2*>(sp);
+                rsc[0] = static_cast<uint16_t>(v.x);
+                rsc[1] = static_cast<uint16_t>(v.x >> 16);
+                rsc[2] = static_cast<uint16_t>(v.y);
+                rsc[3] = static_cast<uint16_t>(v.y >> 16);
+            }
+        }
     };
     auto store_a = [&](int buf) {
 #pragma unroll
@@ -177,15 +214,29 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
             *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0[i]]) = frag2(ra[i].x, ra[i].y);
             *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1[i]]) = frag2(ra[i].z, ra[i].w);
         }
-        if constexpr (MODE != kDump) st[buf].scale[tid] = rsc;
+        if constexpr (MODE != kDump) {
+#pragma unroll
+            for (int gi = 0; gi < GPS; ++gi) st[buf].scale[gi][tid] = rsc[gi];
+        }
     };
+    // w[j][kk / 2] holds the two packed dwords of MFMA kk (x, y for even kk, z, w for odd)
     uint4 w[NJ][2];
     auto load_w = [&](int ks) {
         const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2);
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-            w[j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
-            w[j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
+            if constexpr (FINE) {
+                // MFMA kk, lane half h: packed bytes 16 kk + 8 h .. + 7
+                const uint2 q0 = *reinterpret_cast<const uint2*>(base + w_off[j]);
+                const uint2 q1 = *reinterpret_cast<const uint2*>(base + w_off[j] + 16);
+                const uint2 q2 = *reinterpret_cast<const uint2*>(base + w_off[j] + 32);
+                const uint2 q3 = *reinterpret_cast<const uint2*>(base + w_off[j] + 48);
+                w[j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+                w[j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+            } else {
+                w[j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
+                w[j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
+            }
         }
     };
 
@@ -208,14 +259,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
             af[kk] = *reinterpret_cast<const i32x4*>(&st[buf].a[row * AROW + (2 * kk + lh) * 16]);
     };
     // Weight scales of this lane's 16 columns in block j (binary16 pairs).
-    auto read_sw = [&](int buf, int j, uint2 (&swh)[4]) {
+    auto read_sw = [&](int buf, int j, uint2 (&swh)[4], int gi = 0) {
         const int c = BM + wn * NJ * 32 + j * 32 + 4 * lh;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[buf].scale[c + 8 * q]);
+        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[buf].scale[gi][c + 8 * q]);
     };
     // Activation scale of this lane's row in block i, with the 1/256 of the widening.
-    auto read_sa = [&](int buf, int i) {
-        return h2f(st[buf].scale[wm * MI * 32 + i * 32 + l32]) * (1.0f / 256.0f);
+    auto read_sa = [&](int buf, int i, int gi = 0) {
+        return h2f(st[buf].scale[gi][wm * MI * 32 + i * 32 + l32]) * (1.0f / 256.0f);
     };
     auto sw_at = [](const uint2 (&swh)[4], int r) {
         const uint32_t pair = (r & 2) ? swh[r >> 2].y : swh[r >> 2].x;
@@ -276,6 +327,62 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         }
     };
 
+    // Exact group sums of block (i, j) for group g (dump mode).
+    auto dump_block = [&](const i32x16& d, int i, int j, int g) {
+        const int gm = m0 + wm * MI * 32 + i * 32 + l32;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+            const int v = MAGIC_OK ? (d[r] - static_cast<int>(MAGIC_BITS)) : d[r];
+            if (gm < M && gn < N) P[(static_cast<int64_t>(gm) * N + gn) * ng + g] = v >> 8;
+        }
+    };
+
+    // One K stage holding GPS whole groups (G < 128): for each group and row
+    // block, KPG MFMAs from the bias, then dequantize (or dump) right away.
+    auto compute_fine = [&](int buf, int next, int ks) __attribute__((always_inline)) {
+        i32x4 bw[NJ][KK];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const uint4& v = w[j][kk >> 1];
+                bw[j][kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
+            }
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(next);
+        __builtin_amdgcn_sched_barrier(0);
+        constexpr int NF = GPS * MI;
+        i32x4 af[2][KPG];
+        auto read_f = [&](int f, i32x4 (&dst)[KPG]) __attribute__((always_inline)) {
+            const int gi = f / MI, i = f % MI;
+            const int row = wm * MI * 32 + i * 32 + l32;
+#pragma unroll
+            for (int q = 0; q < KPG; ++q)
+                dst[q] = *reinterpret_cast<const i32x4*>(&st[buf].a[row * AROW + (2 * (gi * KPG + q) + lh) * 16]);
+        };
+        read_f(0, af[0]);
+        uint2 swh[NJ][4];
+        static_for<0, NF>([&](auto F) __attribute__((always_inline)) {
+            constexpr int f = decltype(F)::value;
+            constexpr int gi = f / MI, i = f % MI;
+            if constexpr (f + 1 < NF) read_f(f + 1, af[(f + 1) & 1]);
+            if constexpr (MODE == kRotate && i == 0) {
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) read_sw(buf, j, swh[j], gi);
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                i32x16 d = start;
+#pragma unroll
+                for (int q = 0; q < KPG; ++q)
+                    d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][gi * KPG + q], af[f & 1][q], d, 0, 0, 0);
+                if constexpr (MODE == kRotate) dequant(d, acc[i][j], read_sa(buf, i, gi), swh[j]);
+                else dump_block(d, i, j, ks * GPS + gi);
+            }
+        });
+    };
+
     // End of a group for the persistent modes.
     auto finish_group = [&](int buf, int g) {
         if constexpr (MODE == kPersist) {
@@ -311,7 +418,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         constexpr int buf = decltype(BUF)::value;
         const int ahead = min(ks + 1, nks - 1);
         load_a(ahead);
-        if constexpr (ROTATE) {
+        if constexpr (FINE) {
+            compute_fine(buf, ahead, ks);
+        } else if constexpr (ROTATE) {
             compute(buf, ahead, std::true_type{});
         } else {
             if ((ks % spg) == 0) compute(buf, ahead, std::true_type{});
@@ -377,13 +486,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     }
 }
 
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK>
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
 hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                   int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK>), dim3(static_cast<unsigned>(tiles)),
+    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS>), dim3(static_cast<unsigned>(tiles)),
                        dim3(64 * WAVES_M * WAVES_N), 0, stream, Aq, sa, Wq, sw, static_cast<int>(M),
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
     return hipGetLastError();
@@ -399,10 +508,14 @@ template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                         int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
     if (P) {
+        if (G == 32) return launch<1, WAVES_N, MI, 1, kDump, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+        if (G == 64) return launch<1, WAVES_N, MI, 1, kDump, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         if (G <= 256) return launch<1, WAVES_N, MI, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         return launch<1, WAVES_N, MI, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     }
     if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 128) return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);

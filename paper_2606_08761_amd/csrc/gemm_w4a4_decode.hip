@@ -73,7 +73,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const int l32 = lane & 31, lh = lane >> 5;
     const int nks = K / 128;
     const int ng = K / G;
-    const int lg = (G == K) ? 31 : (G == 128 ? 0 : (G == 256 ? 1 : 2));  // group of stage s: s >> lg
+    const int lg = (G == K) ? 31 : (G == 128 ? 0 : (G == 256 ? 1 : (G == 512 ? 2 : 3)));  // group of stage s: s >> lg
     const int ntiles = (N + COLS - 1) / COLS;
     const int my_tiles = static_cast<int>(blockIdx.x) < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
     const int per_tile = (nks + NWAVE - 1) / NWAVE;  // stages per wave per tile (the last may be null)
@@ -237,7 +237,7 @@ int device_cu_count() {
 }
 
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
-    const bool g_ok = G == K || G == 128 || G == 256 || G == 512;
+    const bool g_ok = G == K || G == 128 || G == 256 || G == 512 || G == 1024;
     return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SA_LDS;
 }
 

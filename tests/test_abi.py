@@ -104,7 +104,8 @@ def test_gemm_validation(L):
     assert g(*ok, 4, 0, 256, 128, h.ptr(), s) == -2
     assert g(*ok, 4, 8, 64, 64, h.ptr(), s) == -2                  # K < 128
     assert g(*ok, 4, 8, 320, 64, h.ptr(), s) == -2                 # K % 128
-    assert g(*ok, 4, 8, 256, 64, h.ptr(), s) == -3                 # G not in {128,256,512,K}
+    assert g(*ok, 4, 8, 384, 96, h.ptr(), s) == -3                 # G not in {32,...,1024} and not K
+    assert g(*ok, 4, 8, 4096, 2048, h.ptr(), s) == -3
     assert g(*ok, 4, 8, 1024, 1000, h.ptr(), s) == -3
     assert g(*ok, 4, 8, 384, 256, h.ptr(), s) == -2                # K % G
     assert g(h.ptr(1), *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -4
@@ -131,7 +132,7 @@ def test_linear_validation(L):
     assert f(*args(x=NULL), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -1
     assert f(*args(), 4, 8, 256, 128, h.ptr(), NULL, h.ptr(), s) == -1
     assert f(*args(), 4, 8, 200, 128, h.ptr(), h.ptr(), h.ptr(), s) == -2
-    assert f(*args(), 4, 8, 256, 32, h.ptr(), h.ptr(), h.ptr(), s) == -3
+    assert f(*args(), 4, 8, 384, 96, h.ptr(), h.ptr(), h.ptr(), s) == -3
     assert f(*args(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -4
 
 

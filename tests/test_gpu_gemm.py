@@ -46,6 +46,8 @@ RAGGED = [
     (1, 128, 128, 128), (8, 200, 256, 128), (33, 1024, 1024, 256), (129, 136, 512, 512),
     (2, 64, 1024, 1024), (300, 260, 384, 128), (64, 1024, 1024, 1024), (17, 8, 256, 256),
     (255, 257, 768, 256), (128, 128, 2048, 512), (1, 1, 128, 128), (130, 33, 3072, 3072),
+    (64, 300, 1024, 32), (130, 520, 1536, 64), (3, 40, 512, 32), (200, 264, 4096, 1024),
+    (400, 1000, 2048, 32), (9, 96, 2048, 1024),
 ]
 
 
@@ -60,7 +62,7 @@ def test_ragged_shapes(O, M, N, K, G):
     check_tolerance(run_gemm(Aq, sa, Wq, sw, G), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"ragged {M}x{N}x{K} G{G}")
 
 
-@pytest.mark.parametrize("G", [128, 256, 512])
+@pytest.mark.parametrize("G", [32, 64, 128, 256, 512, 1024])
 def test_extreme_codes(O, G):
     """Every code -8: P = 64 G per group, the largest magnitude the int32 path sees."""
     M, N, K = 40, 72, 1024
@@ -164,7 +166,8 @@ def test_decode_linear(O, N, K):
 
 DECODE = [
     (1, 96, 4224, 128), (5, 40, 2560, 512), (32, 300, 1536, 1536), (16, 64, 28672, 256),
-    (3, 1000, 1152, 128), (31, 33, 640, 128), (32, 8192, 8192, 512),
+    (3, 1000, 1152, 128), (31, 33, 640, 128), (32, 8192, 8192, 512), (8, 520, 8192, 1024),
+    (4, 300, 2048, 64), (32, 1024, 1024, 32),
 ]
 
 
@@ -198,6 +201,25 @@ def test_decode_repeatable():
     Y1 = m.apex4_w4a4_gemm(a, s1, w, s2, G)
     for _ in range(5):
         assert torch.equal(m.apex4_w4a4_gemm(a, s1, w, s2, G), Y1)
+
+
+@pytest.mark.parametrize("G", [32, 64, 1024])
+def test_fine_and_coarse_groups_float_workload(O, G):
+    """The paper's other granularities (Sec. 3.2.2): activations and weights quantized
+    on the device with G, every output element checked; exact group sums on a row window."""
+    M, N, K = 256, 1024, 4096
+    log(f"granularity G={G} M={M} N={N} K={K}")
+    x, w = wl.float_workload("gsweep", M, N, K)
+    m = pk()
+    Aq_d, sa_d = m.apex4_quantize_act(dev(x), G)
+    Wq_d, sw_d = m.apex4_quantize_act(dev(w), G)
+    Aq_o, sa_o = O.quantize(x, G)
+    Wq_o, sw_o = O.quantize(w, G)
+    assert np.array_equal(host(Aq_d), Aq_o) and np.array_equal(host(Wq_d), Wq_o)
+    check_tolerance(host(m.apex4_w4a4_gemm(Aq_d, sa_d, Wq_d, sw_d, G)), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G),
+                    f"G={G}")
+    P = host(m.apex4_w4a4_gemm_groupsums(Aq_d, Wq_d, G, 100, 40))
+    assert np.array_equal(P.astype(np.int64), O.groupsums(Aq_o[100:140], Wq_o, K, G))
 
 
 def test_repeatable_and_degenerate():
