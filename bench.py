@@ -56,7 +56,9 @@ def parse():
     p.add_argument("--stats-csv", help="summarize: kernel_stats.csv of the --kernel-trace --stats run")
     p.add_argument("--commands", help="summarize: text file with the exact commands that made the CSVs")
     p.add_argument("--bench-log", help="summarize: output of the traced bench run (its JSON line)")
-    p.add_argument("--gsweep-trace", help="summarize: kernel_stats.csv of the --kernel-trace --stats run of --mode gsweep")
+    p.add_argument("--gsweep-trace", help="summarize: kernel_trace.csv of the --kernel-trace run of --mode gsweep")
+    p.add_argument("--rho-json", help="summarize: output of --mode rho (written to profiles/rho_probes.md)")
+    p.add_argument("--rho-command", default="python3 bench.py --mode rho", help="summarize: the command that made --rho-json")
     p.add_argument("--gsweep-pmc", help="summarize: counter_collection.csv of the SQ counter pass over --mode gsweep")
     return p.parse_args()
 
@@ -188,41 +190,70 @@ def summarize_mode(args):
         f.write("\n".join(lines) + "\n")
     if args.gsweep_trace and args.gsweep_pmc:
         summarize_gsweep(args.gsweep_trace, args.gsweep_pmc, cmds)
+    if args.rho_json:
+        summarize_rho(args.rho_json, args.rho_command)
     print(json.dumps(prof, indent=1))
 
 
-GSWEEP_MODES = {"0, true": 128, "1, true": 256, "1, false": 512, "2, false": 8192}
+def summarize_rho(path, command):
+    """profiles/rho_probes.md from the rho probe output (shader-clock cycles, no profiler)."""
+    r = json.load(open(path))
+    co = r["mfma_cycles_per_simd_2_waves_v_fma_interleaved"]
+    lines = ["# rho probes on MI355X (intra-CU INT8 MFMA vs fp32 VALU rates)", "",
+             "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
+             "Cycles are shader clocks counted inside the probe kernels (s_memtime); per-SIMD figures use the slowest "
+             "wave of each CU.", "",
+             "| quantity | value |", "|---|---|",
+             f"| cycles per v_mfma_i32_32x32x32_i8 (1 wave/SIMD) | {r['cycles_per_mfma_i32_32x32x32_i8']:.2f} |",
+             f"| INT8 MFMA ops/clk/CU | {r['int8_mfma_ops_per_clk_per_cu']:.0f} |",
+             f"| cycles per v_fma_f32 per SIMD, 2 waves/SIMD | {r['cycles_per_v_fma_f32_per_simd_2_waves']:.2f} |",
+             f"| cycles per v_fma_f32 per SIMD, 4 waves/SIMD | {r['cycles_per_v_fma_f32_per_simd_4_waves']:.2f} |",
+             f"| fp32 flops/clk/CU (sustained) | {r['fp32_fma_flops_per_clk_per_cu_sustained']:.1f} |",
+             f"| rho measured (INT8 MFMA ops / fp32 flops) | {r['rho_measured']:.1f} |",
+             f"| rho datasheet, packed fp32 / unpacked | {r['rho_datasheet_packed_fp32']:.1f} / {r['rho_datasheet_unpacked_fp32']:.1f} |",
+             f"| shader clock of the probe run (MHz) | {r['shader_clock_mhz']:.0f} |", "",
+             "MFMA cycles per SIMD with 2 waves per SIMD, each interleaving V independent v_fma_f32 per MFMA:", "",
+             "| V | " + " | ".join(co) + " |", "|---|" + "---|" * len(co),
+             "| cycles | " + " | ".join(f"{v:.1f}" for v in co.values()) + " |"]
+    with open(os.path.join(ROOT, "profiles", "rho_probes.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def summarize_gsweep(trace_csv, pmc_csv, cmds):
     """profiles/gemm_w4a4_gsweep_m4096.md: per group size, kernel time and the
-    VALU / MFMA instruction counts per wave and group (SQ counters)."""
+    VALU / MFMA instruction counts per wave and group (SQ counters).  GEMM
+    dispatches are assigned to group sizes by position (GSWEEP_LAUNCHES each, in
+    GSWEEP order)."""
     import csv
     import statistics
-    Mg, Ng, Kg, _ = GSWEEP
+    Mg, Ng, Kg, Gs = GSWEEP
     waves = -(-Mg // 128) * -(-Ng // 256) * 8
 
-    def mode_of(name):
-        m = re.search(r"w4a4_gemm_kernel<1, 8, 4, 1, (\d, (?:true|false))>", name)
-        return GSWEEP_MODES.get(m.group(1)) if m else None
+    def by_position(ids):
+        ids = sorted(ids)
+        assert len(ids) == GSWEEP_LAUNCHES * len(Gs), (len(ids), "GEMM dispatches")
+        return {d: Gs[i // GSWEEP_LAUNCHES] for i, d in enumerate(ids)}
 
-    times = {}
-    for r in csv.DictReader(open(trace_csv)):
-        g = mode_of(r["Name"])
-        if g:
-            times[g] = float(r["AverageNs"]) / 1e3
+    trace = [r for r in csv.DictReader(open(trace_csv)) if "w4a4_gemm_kernel" in r["Kernel_Name"]]
+    gmap = by_position({int(r["Dispatch_Id"]) for r in trace})
+    durs = {}
+    for r in trace:
+        durs.setdefault(gmap[int(r["Dispatch_Id"])], []).append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    times = {g: statistics.median(v) for g, v in durs.items()}
+    rows = [r for r in csv.DictReader(open(pmc_csv)) if "w4a4_gemm_kernel" in r["Kernel_Name"]]
+    pmap = by_position({int(r["Dispatch_Id"]) for r in rows})
     cnt = {}
-    for r in csv.DictReader(open(pmc_csv)):
-        g = mode_of(r["Kernel_Name"])
-        if g:
-            cnt.setdefault(g, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    for r in rows:
+        cnt.setdefault(pmap[int(r["Dispatch_Id"])], {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     c = {g: {k: statistics.mean(v) for k, v in d.items()} for g, d in cnt.items()}
     base_valu = c[Kg]["SQ_INSTS_VALU"]
     lines = [f"# W4A4 GEMM granularity sweep, M={Mg} N=K={Ng}: rocprofv3 summary", "",
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
              "Per group and wave (one wave owns 128 x 32 outputs): MFMA cycles = MFMAs x 32 (v_mfma_i32_32x32x32_i8); "
              "dequant VALU cycles = (VALU instructions - those at G=K) x 4 (one wave64 VALU instruction per 4 SIMD cycles, "
-             "measured). TOPS = 2MNK / average kernel time (kernel trace).", "",
+             "measured). TOPS = 2MNK / median kernel time (kernel trace). For G < 128 a wave's group covers "
+             "128/G times fewer MFMAs, so per-group counts are per the wave's 128 x 32 tile either way.", "",
              "| G | kernel us | TOPS | % INT8 peak | VALU/MFMA (instructions) | MFMA/wave/group | dequant VALU/wave/group "
              "| MFMA cycles/group | dequant VALU cycles/group | VALU/MFMA cycles |",
              "|---|---|---|---|---|---|---|---|---|---|"]
@@ -265,13 +296,15 @@ def counters_mode():
                       "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
 
 
-GSWEEP = (4096, 8192, 8192, (128, 256, 512, 8192))
+GSWEEP = (4096, 8192, 8192, (32, 64, 128, 256, 512, 1024, 8192))
+GSWEEP_LAUNCHES = 23   # per group size: 3 warm-up + 20 timed
 
 
 def gsweep_mode(reps: int = 20):
-    """Granularity sweep (the paper's rho-aware group-size choice): M=4096,
-    N=K=8192, G in {128, 256, 512, K}, random codes and scales.  Each G runs its
-    own kernel mode, so per-kernel counters separate by kernel name."""
+    """Granularity sweep (the paper's rho-aware group-size choice, Sec. 3.2.2):
+    M=4096, N=K=8192, G in {32, 64, 128, 256, 512, 1024, K}, random codes and
+    scales.  Exactly GSWEEP_LAUNCHES GEMM launches per G, in this order, so
+    per-dispatch profiler records map to G by position."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import workloads as wl
@@ -281,7 +314,7 @@ def gsweep_mode(reps: int = 20):
     for Gg in Gs:
         c = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("gsweep", Mg, Ng, Kg, Gg)]
         Y = torch.empty((Mg, Ng), dtype=torch.float16, device=dev)
-        for _ in range(3):
+        for _ in range(GSWEEP_LAUNCHES - reps):
             pk.apex4_w4a4_gemm(*c, Gg, Y)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
@@ -292,7 +325,7 @@ def gsweep_mode(reps: int = 20):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / reps * 1e3
         print(json.dumps({"mode": "gsweep", "M": Mg, "N": Ng, "K": Kg, "G": Gg, "us": round(us, 2),
-                          "tops": round(2.0 * Mg * Ng * Kg / us / 1e6, 1), "launches": reps + 3}), flush=True)
+                          "tops": round(2.0 * Mg * Ng * Kg / us / 1e6, 1), "launches": GSWEEP_LAUNCHES}), flush=True)
         del c, Y
 
 
