@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep"), default="bench",
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power"), default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
                         "summarize: turn rocprofv3 CSV output into the profiles/ summaries")
@@ -60,6 +60,10 @@ def parse():
     p.add_argument("--rho-json", help="summarize: output of --mode rho (written to profiles/rho_probes.md)")
     p.add_argument("--rho-command", default="python3 bench.py --mode rho", help="summarize: the command that made --rho-json")
     p.add_argument("--gsweep-pmc", help="summarize: counter_collection.csv of the SQ counter pass over --mode gsweep")
+    p.add_argument("--sq-csv", nargs="*", help="summarize: counter_collection.csv files of SQ counter passes over --mode counters")
+    p.add_argument("--sq-commands", help="summarize: text file with the commands that made --sq-csv")
+    p.add_argument("--power-log", help="summarize: output of --mode power (written to profiles/power_clock_paper_shape.md)")
+    p.add_argument("--power-command", default="python3 bench.py --mode power", help="summarize: the command that made --power-log")
     return p.parse_args()
 
 
@@ -128,6 +132,14 @@ def summarize_mode(args):
         xs = [v for k, vs in vals.items() if key in k for v in vs]
         return statistics.mean(xs) if xs else None
 
+    if not (args.fetch_csv and args.write_csv and args.stats_csv):
+        if args.sq_csv:
+            summarize_sq(args.sq_csv, open(args.sq_commands).read().strip() if args.sq_commands else "")
+        if args.power_log:
+            summarize_power(args.power_log, args.power_command)
+        if args.rho_json:
+            summarize_rho(args.rho_json, args.rho_command)
+        return
     copy_kib = (256 << 20) / 1024.0
     fetch = per_kernel(args.fetch_csv, "FETCH_SIZE")
     write = per_kernel(args.write_csv, "WRITE_SIZE")
@@ -192,7 +204,145 @@ def summarize_mode(args):
         summarize_gsweep(args.gsweep_trace, args.gsweep_pmc, cmds)
     if args.rho_json:
         summarize_rho(args.rho_json, args.rho_command)
+    if args.sq_csv:
+        summarize_sq(args.sq_csv, open(args.sq_commands).read().strip() if args.sq_commands else "")
+    if args.power_log:
+        summarize_power(args.power_log, args.power_command)
     print(json.dumps(prof, indent=1))
+
+
+def summarize_sq(paths, cmds):
+    """profiles/gemm_w4a4_sq_paper_shape.md: where the SIMD cycles of the
+    paper-shape G=128 GEMM go, from SQ counters (means over the GEMM dispatches
+    of bench.py --mode counters).  Quad-cycle counters are multiplied by 4;
+    per-SIMD figures divide by the 1024 SIMDs; the kernel's cycle count is
+    GRBM_GUI_ACTIVE over the 8 XCDs."""
+    import csv
+    import statistics
+    vals = {}
+    for p in paths:
+        for r in csv.DictReader(open(p)):
+            if "w4a4_gemm_kernel" not in r["Kernel_Name"]:
+                continue
+            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    c = {k: statistics.mean(v) for k, v in vals.items()}
+    simds = 1024
+    kcyc = c["GRBM_GUI_ACTIVE"] / 8
+    quad = ["SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_VALU2",
+            "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA", "SQ_ACTIVE_INST_MISC", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+            "SQ_WAIT_INST_LDS"]
+    plain = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT"]
+    mf = c["SQ_INSTS_MFMA"] / simds
+    lines = [f"# W4A4 GEMM, M={M} N=K={N} G={G}: SQ counters (where the SIMD cycles go)", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
+             f"Kernel length: GRBM_GUI_ACTIVE / 8 XCDs = {kcyc:.0f} cycles. Per SIMD: {mf:.0f} MFMA "
+             f"(v_mfma_i32_32x32x32_i8), {c['SQ_INSTS_VALU'] / simds:.0f} VALU "
+             f"({c['SQ_INSTS_VALU'] / c['SQ_INSTS_MFMA']:.2f} per MFMA), {c['SQ_INSTS_LDS'] / simds:.0f} LDS, "
+             f"{c.get('SQ_INSTS_SALU', 0) / simds:.0f} SALU instructions; {kcyc / mf:.1f} cycles per MFMA per SIMD "
+             f"(32 at the MFMA peak).", "",
+             "| counter | per SIMD (cycles) | share of kernel cycles |", "|---|---|---|"]
+    for k in quad:
+        if k in c:
+            v = c[k] * 4 / simds
+            lines.append(f"| {k} (quad-cycles x 4) | {v:.0f} | {v / kcyc:.3f} |")
+    for k in plain:
+        if k in c:
+            v = c[k] / simds
+            lines.append(f"| {k} | {v:.0f} | {v / kcyc:.3f} |")
+    busy = (c["SQ_ACTIVE_INST_VALU"] * 4 + c["SQ_VALU_MFMA_BUSY_CYCLES"] - c["SQ_VALU_MFMA_COEXEC_CYCLES"]) / simds
+    lines += ["", f"* cycles with a VALU or MFMA instruction executing (VALU + MFMA - co-executed): {busy:.0f} "
+                  f"({busy / kcyc:.2f} of the kernel); VALU alone {c['SQ_ACTIVE_INST_VALU'] * 4 / simds / kcyc:.2f}, "
+                  f"MFMA alone {c['SQ_VALU_MFMA_BUSY_CYCLES'] / simds / kcyc:.2f}",
+              f"* VALU cycles per VALU instruction: {c['SQ_ACTIVE_INST_VALU'] * 4 / c['SQ_INSTS_VALU']:.2f}",
+              "", "Raw means per dispatch:", "", "| counter | value |", "|---|---|"]
+    lines += [f"| {k} | {c[k]:.4g} |" for k in sorted(c)]
+    with open(os.path.join(ROOT, "profiles", "gemm_w4a4_sq_paper_shape.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def summarize_power(path, command):
+    """profiles/power_clock_paper_shape.md from the --mode power output."""
+    rows = [json.loads(l) for l in open(path) if l.startswith("{")]
+    lines = ["# Board power and shader clock under sustained GEMM load (M=2048, N=K=8192)", "",
+             "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
+             "Each kernel is launched back to back for about 3 s while amd-smi is sampled every 0.1 s "
+             "(samples in the first 0.7 s are dropped). MI355X's board power limit is 1400 W; its peak "
+             "shader clock is 2400 MHz.", "",
+             "| kernel | us per launch | TOPS (2MNK/t) | socket power W (median) | mean gfx clock MHz (median) | samples |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['kernel']} | {r['us']} | {r['tops']} | {r['power_w']} | {r['clock_mhz']} | {r['samples']} |")
+    with open(os.path.join(ROOT, "profiles", "power_clock_paper_shape.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def power_mode(secs: float = 3.0):
+    """Back-to-back launches of the paper-shape GEMMs for `secs` each while
+    amd-smi samples socket power and the per-XCD gfx clocks."""
+    import statistics
+    import subprocess
+    import threading
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+
+    def sample():
+        try:
+            r = subprocess.run(["amd-smi", "metric", "-g", "0", "-p", "-c", "--json"], capture_output=True,
+                               text=True, timeout=10)
+            d = json.loads(r.stdout)
+            g = d[0] if isinstance(d, list) else d["gpu_data"][0]
+            pw = float(g["power"]["socket_power"]["value"])
+            clks = [float(v["clk"]["value"]) for k, v in g["clock"].items()
+                    if k.startswith("gfx_") and isinstance(v, dict) and isinstance(v.get("clk"), dict)]
+            return pw, statistics.mean(clks) if clks else float("nan")
+        except Exception:  # amd-smi missing or its format differs: no sample
+            return None
+
+    dev = torch.device("cuda", 0)
+    cases = []
+    for Gp in (G, K):
+        c = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("paper", M, N, K, Gp)]
+        Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+        cases.append((f"W4A4 GEMM G={Gp}", (lambda c=c, Y=Y, Gp=Gp: pk.apex4_w4a4_gemm(*c, Gp, Y))))
+    a8 = torch.randint(-128, 127, (M, K), dtype=torch.int8, device=dev)
+    b8 = torch.randint(-128, 127, (K, N), dtype=torch.int8, device=dev)
+    cases.append(("int8 GEMM, torch._int_mm (hipBLASLt), no scales", lambda: torch._int_mm(a8, b8)))
+    x = torch.randn(M, K, dtype=torch.float16, device=dev)
+    w = torch.randn(N, K, dtype=torch.float16, device=dev)
+    cases.append(("fp16 GEMM, torch.matmul (hipBLASLt)", lambda: torch.matmul(x, w.t())))
+    for name, fn in cases:
+        fn()
+        torch.cuda.synchronize()
+        got, stop = [], [False]
+
+        def loop():
+            t0 = time.time()
+            while not stop[0]:
+                s_ = sample()
+                if s_ is not None and time.time() - t0 > 0.7:
+                    got.append(s_)
+                time.sleep(0.1)
+
+        th = threading.Thread(target=loop)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        th.start()
+        n, t0 = 0, time.time()
+        e0.record()
+        while time.time() - t0 < secs:
+            for _ in range(20):
+                fn()
+            n += 20
+            torch.cuda.synchronize()
+        e1.record()
+        torch.cuda.synchronize()
+        stop[0] = True
+        th.join()
+        us = e0.elapsed_time(e1) / n * 1e3
+        pw = statistics.median([p for p, _ in got]) if got else None
+        ck = statistics.median([c_ for _, c_ in got]) if got else None
+        print(json.dumps({"mode": "power", "kernel": name, "us": round(us, 1), "tops": round(2.0 * M * N * K / us / 1e6),
+                          "power_w": pw, "clock_mhz": None if ck is None else round(ck), "samples": len(got)}), flush=True)
 
 
 def summarize_rho(path, command):
@@ -399,6 +549,8 @@ def main():
         return summarize_mode(args)
     if args.mode == "gsweep":
         return gsweep_mode()
+    if args.mode == "power":
+        return power_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
