@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power"), default="bench",
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers"), default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
                         "summarize: turn rocprofv3 CSV output into the profiles/ summaries")
@@ -64,6 +64,8 @@ def parse():
     p.add_argument("--sq-commands", help="summarize: text file with the commands that made --sq-csv")
     p.add_argument("--power-log", help="summarize: output of --mode power (written to profiles/power_clock_paper_shape.md)")
     p.add_argument("--power-command", default="python3 bench.py --mode power", help="summarize: the command that made --power-log")
+    p.add_argument("--layers-log", help="summarize: output of --mode layers (written to profiles/layer_sweep_llama2_70b.md)")
+    p.add_argument("--layers-command", default="python3 bench.py --mode layers", help="summarize: the command that made --layers-log")
     return p.parse_args()
 
 
@@ -133,6 +135,8 @@ def summarize_mode(args):
         return statistics.mean(xs) if xs else None
 
     if not (args.fetch_csv and args.write_csv and args.stats_csv):
+        if args.layers_log:
+            summarize_layers(args.layers_log, args.layers_command)
         if args.sq_csv:
             summarize_sq(args.sq_csv, open(args.sq_commands).read().strip() if args.sq_commands else "")
         if args.power_log:
@@ -193,11 +197,15 @@ def summarize_mode(args):
                   f"{2.5 * M * K + 2 * M * K / G:.3g} algorithmic bytes)",
                   f"* W4A4 GEMM {M}x{N}x{K} G={G}: {b['gemm_us']:.1f} us ({b['gemm_tops']:.0f} TOPS); "
                   f"fp16 GEMM (hipBLASLt) {b['fp16_gemm_us']:.1f} us",
-                  "", "| decode M | N | K | quantize + GEMM us | GEMM us | GEMM HBM GB/s | fp16 GEMM us | speedup vs fp16 |",
+                  "", "Decode linears: eager = one Python call per launch (partly launch-bound at these sizes); "
+                  "graph = the same calls replayed from a captured graph (GPU time, used for GB/s).", "",
+                  "| decode M | N | K | quantize + GEMM us (eager / graph) | GEMM us (eager / graph) | GEMM HBM GB/s | "
+                  "fp16 GEMM us (eager) | speedup vs fp16 (eager / graph) |",
                   "|---|---|---|---|---|---|---|---|"]
         for d in b.get("decode", []):
-            lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d['linear_us']} | {d['gemm_us']} | {d['gemm_hbm_gbs']} | "
-                         f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} |")
+            lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d['linear_us']} / {d.get('linear_graph_us')} | "
+                         f"{d['gemm_us']} / {d.get('gemm_graph_us')} | {d['gemm_hbm_gbs']} | "
+                         f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} / {d.get('speedup_linear_graph_vs_fp16')} |")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     if args.gsweep_trace and args.gsweep_pmc:
@@ -209,6 +217,105 @@ def summarize_mode(args):
     if args.power_log:
         summarize_power(args.power_log, args.power_command)
     print(json.dumps(prof, indent=1))
+
+
+# Llama-2-70B decoder-layer linears (hidden 8192, 64 query heads and 8 KV heads of
+# 128, FFN 28672): (name, N, K, G) with G = 0 meaning per-channel (G = K).  "g128"
+# is the paper's uniform configuration; "mix" its mixed granularity (Sec. 3.2.2):
+# G = 32 for the value and down projections, per-channel for every other linear.
+LAYER_CONFIGS = {
+    "g128": [("qkv", 10240, 8192, 128), ("o", 8192, 8192, 128), ("gate_up", 57344, 8192, 128),
+             ("down", 8192, 28672, 128)],
+    "mix": [("qk", 9216, 8192, 0), ("v", 1024, 8192, 32), ("o", 8192, 8192, 0), ("gate_up", 57344, 8192, 0),
+            ("down", 8192, 28672, 32)],
+}
+LAYER_M = (16, 256, 4096)
+
+
+def layers_mode(reps: int = 10):
+    """The linears of one Llama-2-70B decoder layer under the uniform G=128 and the
+    mixed configuration, each linear timed as quantize + W4A4 GEMM from fp16
+    activations (apex4_w4a4_linear), next to fp16 GEMMs of the same shapes
+    (torch.matmul -> hipBLASLt).  Weights are rotated over copies larger than the
+    Infinity Cache; codes and scales are random (speed does not depend on values)."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    r = wl.rng_for("llama70b", 99)
+
+    def timed(fn, n):
+        for i in range(2):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(n):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3
+
+    for cfg, linears in LAYER_CONFIGS.items():
+        wsets = {}
+        for name, Nl, Kl, Gl in linears:
+            Gv = Gl or Kl
+            Wq = torch.from_numpy(wl.random_codes(r, Nl, Kl)).to(dev)
+            sw = torch.from_numpy(wl.random_scales(r, Nl, Kl // Gv)).to(dev)
+            wsets[name] = [(Wq, sw)] + [(Wq.clone(), sw.clone()) for _ in range(1)]
+        for Ml in LAYER_M:
+            per = {}
+            for name, Nl, Kl, Gl in linears:
+                Gv = Gl or Kl
+                x = torch.from_numpy(wl.activations(wl.rng_for("llama70b", 98, Ml + Kl), Ml, Kl)).to(dev)
+                Y = torch.empty((Ml, Nl), dtype=torch.float16, device=dev)
+                Aq = torch.empty((Ml, Kl // 2), dtype=torch.uint8, device=dev)
+                sa = torch.empty((Ml, Kl // Gv), dtype=torch.float16, device=dev)
+                ws = wsets[name]
+                per[name] = round(timed(lambda i: pk.apex4_w4a4_linear(x, ws[i % 2][0], ws[i % 2][1], Gv, Y, Aq, sa),
+                                        reps), 2)
+                del x, Y, Aq, sa
+            print(json.dumps({"mode": "layers", "config": cfg, "M": Ml, "linear_us": per,
+                              "total_us": round(sum(per.values()), 2)}), flush=True)
+        del wsets
+        torch.cuda.empty_cache()
+    # fp16 GEMMs of the same shapes (the value projection is part of qkv)
+    shapes = [("qkv", 10240, 8192), ("o", 8192, 8192), ("gate_up", 57344, 8192), ("down", 8192, 28672)]
+    wf = {n: [torch.randn(Nl, Kl, dtype=torch.float16, device=dev) * 0.02 for _ in range(2)] for n, Nl, Kl in shapes}
+    for Ml in LAYER_M:
+        per = {}
+        for name, Nl, Kl in shapes:
+            x = torch.randn(Ml, Kl, dtype=torch.float16, device=dev)
+            Y = torch.empty((Ml, Nl), dtype=torch.float16, device=dev)
+            per[name] = round(timed(lambda i: torch.matmul(x, wf[name][i % 2].t(), out=Y), reps), 2)
+        print(json.dumps({"mode": "layers", "config": "fp16", "M": Ml, "linear_us": per,
+                          "total_us": round(sum(per.values()), 2)}), flush=True)
+
+
+def summarize_layers(path, command):
+    """profiles/layer_sweep_llama2_70b.md from the --mode layers output."""
+    rows = [json.loads(l) for l in open(path) if l.startswith("{")]
+    tot = {(r["config"], r["M"]): r for r in rows}
+    lines = ["# Llama-2-70B decoder-layer linears: uniform G=128 vs mixed granularity vs fp16", "",
+             "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
+             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear), "
+             "weights rotated over 2 copies; fp16 is torch.matmul (hipBLASLt) on the same shapes. "
+             "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
+             "share one per-channel GEMM (N=9216).", "",
+             "| M | g128 us | mix us | fp16 us | g128 speedup vs fp16 | mix speedup vs fp16 |",
+             "|---|---|---|---|---|---|"]
+    for Ml in sorted({r["M"] for r in rows}):
+        g, mx, f = tot.get(("g128", Ml)), tot.get(("mix", Ml)), tot.get(("fp16", Ml))
+        if not (g and mx and f):
+            continue
+        lines.append(f"| {Ml} | {g['total_us']} | {mx['total_us']} | {f['total_us']} | "
+                     f"{f['total_us'] / g['total_us']:.2f} | {f['total_us'] / mx['total_us']:.2f} |")
+    lines += ["", "Per linear (us):", "", "| config | M | per linear |", "|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['config']} | {r['M']} | " + ", ".join(f"{k} {v}" for k, v in r["linear_us"].items()) + " |")
+    with open(os.path.join(ROOT, "profiles", "layer_sweep_llama2_70b.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def summarize_sq(paths, cmds):
@@ -488,6 +595,9 @@ def decode_bench(reps: int = 50):
     Weight copies are rotated past the 256 MB Infinity Cache.  Algorithmic bytes of
     the GEMM: M K/2 + N K/2 + 2 (M + N) K/G + 2 M N; the linear adds the fp16 x
     (2 M K).  Also times the fp16 GEMM of the same shape (torch -> hipBLASLt).
+    Each W4A4 call is timed twice: eager (one Python call per launch, which at
+    these sizes is partly launch-bound) and as a replayed graph of the same
+    calls (GPU time; the HBM rates use it).
     """
     import torch
     import paper_2606_08761_amd as pk
@@ -525,16 +635,49 @@ def decode_bench(reps: int = 50):
             torch.cuda.synchronize()
             return e0.elapsed_time(e1) / reps * 1e3
 
-        lin_us = timed(lambda i: pk.apex4_w4a4_linear(x, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y, Aq, sa))
-        gemm_us = timed(lambda i: pk.apex4_w4a4_gemm(Aq, sa, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y))
+        def graph_timed(fn, out):
+            """GPU time per call without the Python launch overhead: `reps` calls
+            captured in one graph, replayed; the replayed output must equal the
+            eager output bit for bit (the kernels are deterministic)."""
+            fn(reps - 1)
+            torch.cuda.synchronize()
+            ref = out.clone()
+            side = torch.cuda.Stream(dev)
+            side.wait_stream(stream)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                for i in range(reps):
+                    fn(i)
+            out.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            if not torch.equal(out, ref):
+                raise RuntimeError("graph replay differs from the eager result")
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            del g
+            return e0.elapsed_time(e1) / reps * 1e3
+
+        lin = lambda i: pk.apex4_w4a4_linear(x, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y, Aq, sa)
+        gem = lambda i: pk.apex4_w4a4_gemm(Aq, sa, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y)
+        lin_us = timed(lin)
+        gemm_us = timed(gem)
+        lin_g_us = graph_timed(lin, Y)
+        gemm_g_us = graph_timed(gem, Y)
         yf = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
         fp16_us = timed(lambda i: torch.matmul(x, fsets[i % len(fsets)].t(), out=yf))
         gbytes = Md * Kd / 2 + Nd * Kd / 2 + 2 * (Md + Nd) * Kd / Gd + 2 * Md * Nd
         out.append({"M": Md, "N": Nd, "K": Kd, "G": Gd, "linear_us": round(lin_us, 2), "gemm_us": round(gemm_us, 2),
-                    "gemm_hbm_gbs": round(gbytes / (gemm_us * 1e-6) / 1e9, 1),
-                    "gemm_hbm_frac": round(gbytes / (gemm_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
-                    "linear_hbm_gbs": round((gbytes + 2 * Md * Kd) / (lin_us * 1e-6) / 1e9, 1),
-                    "fp16_gemm_us": round(fp16_us, 2), "speedup_linear_vs_fp16": round(fp16_us / lin_us, 3)})
+                    "linear_graph_us": round(lin_g_us, 2), "gemm_graph_us": round(gemm_g_us, 2),
+                    "gemm_hbm_gbs": round(gbytes / (gemm_g_us * 1e-6) / 1e9, 1),
+                    "gemm_hbm_frac": round(gbytes / (gemm_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
+                    "linear_hbm_gbs": round((gbytes + 2 * Md * Kd) / (lin_g_us * 1e-6) / 1e9, 1),
+                    "fp16_gemm_us": round(fp16_us, 2), "speedup_linear_vs_fp16": round(fp16_us / lin_us, 3),
+                    "speedup_linear_graph_vs_fp16": round(fp16_us / lin_g_us, 3)})
         del x, Aq, sa, Y, yf
     wcache.clear()
     torch.cuda.synchronize()
@@ -551,6 +694,8 @@ def main():
         return gsweep_mode()
     if args.mode == "power":
         return power_mode()
+    if args.mode == "layers":
+        return layers_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)

@@ -23,6 +23,11 @@
 //     1.5 * 2^23 accumulator bias gives the float conversion for free at every G.
 //     The weight scale is one value per lane.  The activation scales of all rows
 //     and groups (at most 32 * K/G binary16) sit in LDS for the whole kernel.
+//   * Groups of 32 or 64 (GPS = 4 or 2 groups per 128-wide stage): each MFMA
+//     must stay inside one group, so lane half h of MFMA kk covers
+//     k in [32 kk + 16 h, 32 kk + 16 h + 16) (packed bytes 16 kk + 8 h .. + 7)
+//     for both operands, and every group's MFMAs start from the bias and are
+//     dequantized with that group's scales.
 //   * The 8 partial fp32 tiles are summed through LDS in a fixed order and
 //     rounded once to binary16.
 #include <hip/hip_fp16.h>
@@ -58,9 +63,10 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
 }
 
 // MROWS in {8, 16, 32}: the rows that can hold outputs (M <= MROWS); only they
-// are dequantized and reduced.  PF: stages in flight per wave.  Lane l holds rows 8 (r / 4) + 4 (l / 32) + r % 4
-// for r < MROWS / 2.
-template <int MROWS, int PF>
+// are dequantized and reduced.  PF: stages in flight per wave.  GPS: groups per
+// 128-wide stage (1 for G >= 128, 2 for G = 64, 4 for G = 32).  Lane l holds
+// rows 8 (r / 4) + 4 (l / 32) + r % 4 for r < MROWS / 2.
+template <int MROWS, int PF, int GPS>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
@@ -73,41 +79,92 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const int l32 = lane & 31, lh = lane >> 5;
     const int nks = K / 128;
     const int ng = K / G;
-    const int lg = (G == K) ? 31 : (G == 128 ? 0 : (G == 256 ? 1 : (G == 512 ? 2 : 3)));  // group of stage s: s >> lg
+    // group of stage s (GPS == 1): s >> lg; first group of stage s (GPS > 1): s * GPS
+    const int lg = (G == K) ? 31 : (G <= 128 ? 0 : (G == 256 ? 1 : (G == 512 ? 2 : 3)));
+    constexpr int KPG = 4 / GPS;       // MFMAs per group and stage
     const int ntiles = (N + COLS - 1) / COLS;
     const int my_tiles = static_cast<int>(blockIdx.x) < ntiles ? (ntiles - 1 - blockIdx.x) / gridDim.x + 1 : 0;
     const int per_tile = (nks + NWAVE - 1) / NWAVE;  // stages per wave per tile (the last may be null)
     const int total = my_tiles * per_tile;
 
-    // activation scales; rows past M are clamped (their outputs are never stored)
-    for (int i = tid; i < ng * ROWS; i += 64 * NWAVE) {
-        const int r = i / ng, g = i - r * ng;
-        sas[g * ROWS + r] = sa[static_cast<int64_t>(min(r, M - 1)) * ng + g];
+    // activation scales; rows past M are clamped (their outputs are never stored).
+    // Rows of 8k scales are read as 16-byte vectors, four per thread with all
+    // loads issued before the LDS stores, so the staging costs one load latency.
+    if ((ng & 7) == 0) {
+        const int nv = ng >> 3;  // vectors per row
+        constexpr int NT = 64 * NWAVE;
+        for (int i0 = tid; i0 < ROWS * nv; i0 += 4 * NT) {
+            uint4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * NT;
+                if (i < ROWS * nv) {
+                    const int r = i / nv, c = i - r * nv;
+                    v[u] = *reinterpret_cast<const uint4*>(sa + static_cast<int64_t>(min(r, M - 1)) * ng + 8 * c);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * NT;
+                if (i < ROWS * nv) {
+                    const int r = i / nv, c = i - r * nv;
+                    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        sas[(8 * c + e) * ROWS + r] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+                }
+            }
+        }
+    } else {
+        for (int i = tid; i < ng * ROWS; i += 64 * NWAVE) {
+            const int r = i / ng, g = i - r * ng;
+            sas[g * ROWS + r] = sa[static_cast<int64_t>(min(r, M - 1)) * ng + g];
+        }
     }
 
     // per-lane byte offsets; every load adds a wave-uniform base (stage and group)
-    const uint32_t a_voff = static_cast<uint32_t>(min(l32, M - 1)) * static_cast<uint32_t>(K / 2) + 32 * lh;
+    constexpr uint32_t HOFF = GPS > 1 ? 8 : 32;   // byte offset of lane half 1 within a stage
+    const uint32_t a_voff = static_cast<uint32_t>(min(l32, M - 1)) * static_cast<uint32_t>(K / 2) + HOFF * lh;
     uint32_t w_voff = 0, s_voff = 0;
     auto set_tile = [&](int t) {
         const int n = min((static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS + l32, N - 1);
-        w_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + 32 * lh;
+        w_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + HOFF * lh;
         s_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(ng);
     };
 
     // ring of in-flight stages; (lt, li) is the next (tile, stage) to load.  No
     // load is issued past the last stage.
     uint4 rw[PF][2], ra[PF][2];
-    uint32_t rs[PF];
+    uint2 rs[PF];   // weight scales of the stage's groups (binary16, GPS of them)
     int lt = 0, li = 0;
+    // 32 packed bytes of one lane for a stage: two 16-byte runs (GPS == 1), or
+    // four 8-byte pieces 16 apart (one per MFMA) when groups are finer than a stage
+    auto load32 = [](const uint8_t* p, uint4 (&r)[2]) __attribute__((always_inline)) {
+        if constexpr (GPS == 1) {
+            r[0] = *reinterpret_cast<const uint4*>(p);
+            r[1] = *reinterpret_cast<const uint4*>(p + 16);
+        } else {
+            const uint2 q0 = *reinterpret_cast<const uint2*>(p);
+            const uint2 q1 = *reinterpret_cast<const uint2*>(p + 16);
+            const uint2 q2 = *reinterpret_cast<const uint2*>(p + 32);
+            const uint2 q3 = *reinterpret_cast<const uint2*>(p + 48);
+            r[0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+            r[1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+        }
+    };
     auto load = [&](int j) {
         const int s = min(wave + NWAVE * li, nks - 1);
         const uint8_t* wb = Wq + static_cast<int64_t>(s) * 64;
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
-        rw[j][0] = *reinterpret_cast<const uint4*>(wb + w_voff);
-        rw[j][1] = *reinterpret_cast<const uint4*>(wb + w_voff + 16);
-        ra[j][0] = *reinterpret_cast<const uint4*>(ab + a_voff);
-        ra[j][1] = *reinterpret_cast<const uint4*>(ab + a_voff + 16);
-        rs[j] = (sw + (s >> lg))[s_voff];
+        load32(wb + w_voff, rw[j]);
+        load32(ab + a_voff, ra[j]);
+        if constexpr (GPS == 1) {
+            rs[j].x = (sw + (s >> lg))[s_voff];
+        } else if constexpr (GPS == 2) {
+            rs[j].x = *reinterpret_cast<const uint32_t*>(sw + s_voff + s * 2);
+        } else {
+            rs[j] = *reinterpret_cast<const uint2*>(sw + s_voff + s * 4);
+        }
         if (++li == per_tile) {
             if (lt + 1 < my_tiles) {
                 li = 0;
@@ -133,7 +190,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     auto process = [&](int j) {
         const int s_raw = wave + NWAVE * pi;
         const bool live = s_raw < nks;
-        const int g = min(s_raw, nks - 1) >> lg;
+        const int s = min(s_raw, nks - 1);
         i32x4 bw[4], af[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
@@ -142,22 +199,29 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
             bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             af[kk] = (kk & 1) ? frag2(u.z, u.w) : frag2(u.x, u.y);
         }
-        i32x16 d;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) d[r] = static_cast<int>(MAGIC_BITS);
+        for (int gi = 0; gi < GPS; ++gi) {
+            const int g = GPS == 1 ? (s >> lg) : s * GPS + gi;
+            i32x16 d;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk], bw[kk], d, 0, 0, 0);
-        const float s1 = live ? h2f(static_cast<uint16_t>(rs[j])) * (1.0f / 256.0f) : 0.f;
-        const float nb = -MAGIC * s1;
-        uint2 sah[4];
+            for (int r = 0; r < 16; ++r) d[r] = static_cast<int>(MAGIC_BITS);
 #pragma unroll
-        for (int q4 = 0; q4 < NR / 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
+            for (int q = 0; q < KPG; ++q)
+                d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[gi * KPG + q], bw[gi * KPG + q], d, 0, 0, 0);
+            const uint32_t sword = (gi < 2) ? rs[j].x : rs[j].y;
+            const uint16_t wsc = (gi & 1) ? static_cast<uint16_t>(sword >> 16) : static_cast<uint16_t>(sword & 0xFFFFu);
+            const float s1 = live ? h2f(wsc) * (1.0f / 256.0f) : 0.f;
+            const float nb = -MAGIC * s1;
+            uint2 sah[4];
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            const uint32_t pair = (r & 2) ? sah[r >> 2].y : sah[r >> 2].x;
-            const uint16_t h = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
-            const float tt = fmaf(__int_as_float(d[r]), s1, nb);
-            acc[r] = fmaf(tt, h2f(h), acc[r]);
+            for (int q4 = 0; q4 < NR / 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                const uint32_t pair = (r & 2) ? sah[r >> 2].y : sah[r >> 2].x;
+                const uint16_t h = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
+                const float tt = fmaf(__int_as_float(d[r]), s1, nb);
+                acc[r] = fmaf(tt, h2f(h), acc[r]);
+            }
         }
     };
 
@@ -197,14 +261,14 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     }
 }
 
-template <int PF>
+template <int PF, int GPS>
 hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                             int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
     static bool lds_attr_set = false;  // benign race: every caller sets the same value
     if (!lds_attr_set) {
-        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF>)}) {
+        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS>)}) {
             const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, MAX_SA_LDS);
             if (e != hipSuccess) return e;
         }
@@ -215,9 +279,9 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
     const size_t lds = static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
-    if (M <= 8) hipLaunchKernelGGL((w4a4_decode_kernel<8, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
-    else if (M <= 16) hipLaunchKernelGGL((w4a4_decode_kernel<16, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
-    else hipLaunchKernelGGL((w4a4_decode_kernel<32, PF>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+    if (M <= 8) hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+    else if (M <= 16) hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+    else hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
     return hipGetLastError();
 }
 
@@ -237,14 +301,17 @@ int device_cu_count() {
 }
 
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
-    const bool g_ok = G == K || G == 128 || G == 256 || G == 512 || G == 1024;
+    const bool g_ok = G == K || G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024;
     return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SA_LDS;
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
     if (!decode_fits(M, N, K, G)) return hipErrorInvalidValue;
-    return launch_decode_pf<DECODE_PF>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
+    // four group sums per stage hold more registers: a shorter ring keeps G = 32 spill-free
+    if (G == 32) return launch_decode_pf<DECODE_PF - 2, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
+    if (G == 64) return launch_decode_pf<DECODE_PF, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
+    return launch_decode_pf<DECODE_PF, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
 }
 
 }  // namespace apex4

@@ -168,6 +168,9 @@ DECODE = [
     (1, 96, 4224, 128), (5, 40, 2560, 512), (32, 300, 1536, 1536), (16, 64, 28672, 256),
     (3, 1000, 1152, 128), (31, 33, 640, 128), (32, 8192, 8192, 512), (8, 520, 8192, 1024),
     (4, 300, 2048, 64), (32, 1024, 1024, 32),
+    # G = 32 and 64 on the streaming kernel: the mixed configuration's value
+    # (N=1024, K=8192) and down (K=28672) projections at decode batch sizes
+    (16, 1024, 8192, 32), (16, 2048, 28672, 32), (1, 520, 4096, 64), (9, 96, 8192, 32), (32, 64, 2048, 64),
 ]
 
 
@@ -181,7 +184,7 @@ def test_decode_kernel_shapes(O, M, N, K, G):
     check_tolerance(run_gemm(Aq, sa, Wq, sw, G), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"decode {M}x{N}x{K} G{G}")
 
 
-@pytest.mark.parametrize("G", [128, 512])
+@pytest.mark.parametrize("G", [32, 64, 128, 512])
 def test_decode_extreme_codes(O, G):
     M, N, K = 8, 72, 2048
     Aq = np.full((M, K // 2), 0x88, np.uint8)
