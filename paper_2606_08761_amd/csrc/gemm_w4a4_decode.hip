@@ -45,7 +45,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int NWAVE = 8;
 constexpr int COLS = 32;
 constexpr int ROWS = 32;
-constexpr int MAX_SA_LDS = 64 * 1024;         // bytes of staged activation scales
+constexpr int MAX_SC_LDS = 60 * 1024;         // bytes of each staged scale block ([K/G][32] binary16)
 constexpr int DECODE_PF = 6;                   // stages in flight per wave
 constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
 constexpr float MAGIC = 12582912.0f;
@@ -72,7 +72,9 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
     constexpr int NR = MROWS / 2;      // output registers per lane that matter
     __shared__ float red[NWAVE][NR][64];
-    extern __shared__ uint16_t sas[];  // [K/G][32]: activation scale of row r, group g at g * 32 + r
+    // [K/G][32] twice: activation scale of row r and group g at g * 32 + r, then
+    // the weight scale of the current tile's column c and group g at g * 32 + c
+    extern __shared__ uint16_t sas[];
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -87,55 +89,66 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const int per_tile = (nks + NWAVE - 1) / NWAVE;  // stages per wave per tile (the last may be null)
     const int total = my_tiles * per_tile;
 
-    // activation scales; rows past M are clamped (their outputs are never stored).
-    // Rows of 8k scales are read as 16-byte vectors, four per thread with all
-    // loads issued before the LDS stores, so the staging costs one load latency.
-    if ((ng & 7) == 0) {
-        const int nv = ng >> 3;  // vectors per row
-        constexpr int NT = 64 * NWAVE;
-        for (int i0 = tid; i0 < ROWS * nv; i0 += 4 * NT) {
-            uint4 v[4];
+    // Scales staged in LDS, group-major ([K/G][32]): the activation scales of
+    // rows 0..31 (rows past M clamped; their outputs are never stored) for the
+    // whole kernel, and the weight scales of the current tile's 32 columns
+    // (columns past N clamped).  Rows of 8k scales are read as 16-byte vectors,
+    // four per thread with every load issued before the LDS stores, so a staging
+    // pass costs one load latency.
+    uint16_t* wsc = sas + ng * ROWS;
+    auto stage32 = [&](const uint16_t* base, int rmax, uint16_t* dst) __attribute__((always_inline)) {
+        if ((ng & 7) == 0) {
+            const int nv = ng >> 3;  // vectors per row
+            constexpr int NT = 64 * NWAVE;
+            for (int i0 = tid; i0 < ROWS * nv; i0 += 4 * NT) {
+                uint4 v[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * NT;
-                if (i < ROWS * nv) {
-                    const int r = i / nv, c = i - r * nv;
-                    v[u] = *reinterpret_cast<const uint4*>(sa + static_cast<int64_t>(min(r, M - 1)) * ng + 8 * c);
+                for (int u = 0; u < 4; ++u) {
+                    const int i = i0 + u * NT;
+                    if (i < ROWS * nv) {
+                        const int r = i / nv, c = i - r * nv;
+                        v[u] = *reinterpret_cast<const uint4*>(base + static_cast<int64_t>(min(r, rmax)) * ng + 8 * c);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int i = i0 + u * NT;
+                    if (i < ROWS * nv) {
+                        const int r = i / nv, c = i - r * nv;
+                        const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            dst[(8 * c + e) * ROWS + r] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+                    }
                 }
             }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * NT;
-                if (i < ROWS * nv) {
-                    const int r = i / nv, c = i - r * nv;
-                    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        sas[(8 * c + e) * ROWS + r] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
-                }
+        } else {
+            for (int i = tid; i < ng * ROWS; i += 64 * NWAVE) {
+                const int r = i / ng, g = i - r * ng;
+                dst[g * ROWS + r] = base[static_cast<int64_t>(min(r, rmax)) * ng + g];
             }
         }
-    } else {
-        for (int i = tid; i < ng * ROWS; i += 64 * NWAVE) {
-            const int r = i / ng, g = i - r * ng;
-            sas[g * ROWS + r] = sa[static_cast<int64_t>(min(r, M - 1)) * ng + g];
-        }
-    }
+    };
+    auto tile_col0 = [&](int t) { return (static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS; };
+    auto stage_wscales = [&](int t) __attribute__((always_inline)) {
+        const int c0 = tile_col0(t);
+        stage32(sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
+    };
+    stage32(sa, M - 1, sas);
+    if (my_tiles > 0) stage_wscales(0);
 
     // per-lane byte offsets; every load adds a wave-uniform base (stage and group)
     constexpr uint32_t HOFF = GPS > 1 ? 8 : 32;   // byte offset of lane half 1 within a stage
     const uint32_t a_voff = static_cast<uint32_t>(min(l32, M - 1)) * static_cast<uint32_t>(K / 2) + HOFF * lh;
-    uint32_t w_voff = 0, s_voff = 0;
+    uint32_t w_voff = 0;
     auto set_tile = [&](int t) {
-        const int n = min((static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS + l32, N - 1);
+        const int n = min(tile_col0(t) + l32, N - 1);
         w_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + HOFF * lh;
-        s_voff = static_cast<uint32_t>(n) * static_cast<uint32_t>(ng);
     };
 
     // ring of in-flight stages; (lt, li) is the next (tile, stage) to load.  No
     // load is issued past the last stage.
     uint4 rw[PF][2], ra[PF][2];
-    uint2 rs[PF];   // weight scales of the stage's groups (binary16, GPS of them)
     int lt = 0, li = 0;
     // 32 packed bytes of one lane for a stage: two 16-byte runs (GPS == 1), or
     // four 8-byte pieces 16 apart (one per MFMA) when groups are finer than a stage
@@ -158,13 +171,6 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
         load32(wb + w_voff, rw[j]);
         load32(ab + a_voff, ra[j]);
-        if constexpr (GPS == 1) {
-            rs[j].x = (sw + (s >> lg))[s_voff];
-        } else if constexpr (GPS == 2) {
-            rs[j].x = *reinterpret_cast<const uint32_t*>(sw + s_voff + s * 2);
-        } else {
-            rs[j] = *reinterpret_cast<const uint2*>(sw + s_voff + s * 4);
-        }
         if (++li == per_tile) {
             if (lt + 1 < my_tiles) {
                 li = 0;
@@ -184,7 +190,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
         for (int j = 0; j < PF; ++j) load(j);
     }
-    __syncthreads();  // activation scales staged
+    __syncthreads();  // activation scales and the first tile's weight scales staged
 
     int pi = 0;  // stage-in-tile of the next processed stage
     auto process = [&](int j) {
@@ -208,9 +214,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
             for (int q = 0; q < KPG; ++q)
                 d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[gi * KPG + q], bw[gi * KPG + q], d, 0, 0, 0);
-            const uint32_t sword = (gi < 2) ? rs[j].x : rs[j].y;
-            const uint16_t wsc = (gi & 1) ? static_cast<uint16_t>(sword >> 16) : static_cast<uint16_t>(sword & 0xFFFFu);
-            const float s1 = live ? h2f(wsc) * (1.0f / 256.0f) : 0.f;
+            const float s1 = live ? h2f(wsc[g * ROWS + l32]) * (1.0f / 256.0f) : 0.f;
             const float nb = -MAGIC * s1;
             uint2 sah[4];
 #pragma unroll
@@ -225,12 +229,15 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         }
     };
 
-    // reduce the 8 partial tiles of tile t, store, and clear the accumulator
+    // reduce the 8 partial tiles of tile t, store, clear the accumulator, and
+    // stage the next tile's weight scales (every wave is past tile t's stages
+    // after the first barrier; the second publishes the new scales)
     auto finish_tile = [&](int t) {
 #pragma unroll
         for (int r = 0; r < NR; ++r) red[wave][r][lane] = acc[r];
         __syncthreads();
-        const int n0 = (static_cast<int>(blockIdx.x) + t * static_cast<int>(gridDim.x)) * COLS;
+        if (t + 1 < my_tiles) stage_wscales(t + 1);
+        const int n0 = tile_col0(t);
         for (int o = tid; o < NR * 64; o += 64 * NWAVE) {
             const int r = o >> 6, ln = o & 63;
             float v = 0.f;
@@ -269,14 +276,14 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
         for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS>),
                               reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS>),
                               reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS>)}) {
-            const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, MAX_SA_LDS);
+            const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * MAX_SC_LDS);
             if (e != hipSuccess) return e;
         }
         lds_attr_set = true;
     }
     const int64_t tiles = (N + COLS - 1) / COLS;
     const int64_t grid = tiles < device_cu_count() ? tiles : device_cu_count();
-    const size_t lds = static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
+    const size_t lds = 2 * static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
     if (M <= 8) hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
@@ -302,7 +309,7 @@ int device_cu_count() {
 
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
     const bool g_ok = G == K || G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024;
-    return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SA_LDS;
+    return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SC_LDS;
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
