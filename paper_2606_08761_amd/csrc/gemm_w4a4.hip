@@ -45,7 +45,8 @@
 //     persist over the stages of a group.  G == K: sums persist over all of K
 //     and the scales are applied once in the epilogue.
 //   * Workgroup ids are remapped so that each XCD (8 per MI355X, each with its
-//     own L2) works on a contiguous band of output tiles.
+//     own L2) works on a compact block of output tiles (8 m-tiles by a band of
+//     n-tiles at a time).
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -130,13 +131,30 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     __shared__ Stage<BM, NT, GPS> st[2];
 
     // ---- tile selection (XCD-aware) ----
+    // Workgroup b runs on XCD b & 7 (round-robin dispatch), each XCD with its
+    // own L2.  When both tile counts are multiples of 8, XCD x owns the n-tiles
+    // [x nt/8, (x+1) nt/8) and walks them in bands of 8 m-tiles, so the tiles it
+    // runs at the same time share 8 m-tiles of A and their n-tiles of W (at the
+    // paper shape 4 MB of A + 4 MB of W per XCD and round, instead of all 8 MB
+    // of A + 2 MB of W).  Otherwise XCD x takes a contiguous run of tile ids.
     const int mt_count = (M + BM - 1) / BM;
     const int nt_count = (N + BN - 1) / BN;
     const int T = mt_count * nt_count;
-    int tile = blockIdx.x;
-    if ((T & 7) == 0) tile = (blockIdx.x & 7) * (T >> 3) + (blockIdx.x >> 3);
-    const int m0 = (tile % mt_count) * BM;
-    const int n0 = (tile / mt_count) * BN;
+    int mt, nt;
+    if ((mt_count & 7) == 0 && (nt_count & 7) == 0) {
+        const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+        const int npx = nt_count >> 3;          // n-tiles per XCD
+        const int band = j / (8 * npx), r = j % (8 * npx);
+        mt = band * 8 + (r & 7);
+        nt = x * npx + (r >> 3);
+    } else {
+        int tile = blockIdx.x;
+        if ((T & 7) == 0) tile = (blockIdx.x & 7) * (T >> 3) + (blockIdx.x >> 3);
+        mt = tile % mt_count;
+        nt = tile / mt_count;
+    }
+    const int m0 = mt * BM;
+    const int n0 = nt * BN;
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
