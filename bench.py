@@ -701,8 +701,9 @@ def main():
         print(json.dumps(rho.measure()), flush=True)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on exactly one GPU; --gpus must be 1 "
-              "(the multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        print("bench.py: this benchmark runs on exactly one GPU; --gpus must be 1 "
+              "(the path shards over rows, or over N and K on group boundaries, but no multi-GPU code is built)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
