@@ -134,8 +134,37 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const int c0 = tile_col0(t);
         stage32(sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
     };
-    stage32(sa, M - 1, sas);
-    if (my_tiles > 0) stage_wscales(0);
+    // The next tile's weight scales, when they fit two 16-byte vectors per
+    // thread (K/G <= 256, a multiple of 8): loaded into registers when a tile
+    // starts and written to LDS when it ends, so the tile boundary waits for no
+    // scale load.
+    const bool pf_sc = (ng & 7) == 0 && ng <= 256;
+    uint4 nsc[2];
+    auto prefetch_wscales = [&](int t) __attribute__((always_inline)) {
+        const int c0 = tile_col0(t), nv = ng >> 3;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int i = tid + u * 64 * NWAVE;
+            if (i < ROWS * nv) {
+                const int r = i / nv, c = i - r * nv;
+                nsc[u] = *reinterpret_cast<const uint4*>(sw + static_cast<int64_t>(min(c0 + r, N - 1)) * ng + 8 * c);
+            }
+        }
+    };
+    auto store_wscales = [&]() __attribute__((always_inline)) {
+        const int nv = ng >> 3;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int i = tid + u * 64 * NWAVE;
+            if (i < ROWS * nv) {
+                const int r = i / nv, c = i - r * nv;
+                const uint32_t w[4] = {nsc[u].x, nsc[u].y, nsc[u].z, nsc[u].w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    wsc[(8 * c + e) * ROWS + r] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+            }
+        }
+    };
 
     // per-lane byte offsets; every load adds a wave-uniform base (stage and group)
     constexpr uint32_t HOFF = GPS > 1 ? 8 : 32;   // byte offset of lane half 1 within a stage
@@ -185,11 +214,16 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 
+    // the first stages' loads go out before the scale staging, whose waits then
+    // overlap them: one memory round trip before the first stage is processed
     if (total > 0) {
         set_tile(0);
 #pragma unroll
         for (int j = 0; j < PF; ++j) load(j);
     }
+    stage32(sa, M - 1, sas);
+    if (my_tiles > 0) stage_wscales(0);
+    if (pf_sc && my_tiles > 1) prefetch_wscales(1);
     __syncthreads();  // activation scales and the first tile's weight scales staged
 
     int pi = 0;  // stage-in-tile of the next processed stage
@@ -236,7 +270,10 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
         for (int r = 0; r < NR; ++r) red[wave][r][lane] = acc[r];
         __syncthreads();
-        if (t + 1 < my_tiles) stage_wscales(t + 1);
+        if (t + 1 < my_tiles) {
+            if (pf_sc) store_wscales();
+            else stage_wscales(t + 1);
+        }
         const int n0 = tile_col0(t);
         for (int o = tid; o < NR * 64; o += 64 * NWAVE) {
             const int r = o >> 6, ln = o & 63;
@@ -262,6 +299,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
                 if (++pi == per_tile) {
                     finish_tile(pt++);
                     pi = 0;
+                    if (pf_sc && pt + 1 < my_tiles) prefetch_wscales(pt + 1);
                 }
             }
         }
