@@ -133,6 +133,23 @@ def test_llama70b_linears(O, linear):
         _float_case(O, f"{linear} M={M}", W, x, rows)
 
 
+# The paper's mixed configuration (Sec. 3.2.2) on Llama-2-70B shapes: the value
+# projection (N=1024) and the down projection (K=28672, 896 groups) at G=32, the
+# query+key projection (N=9216) per channel; decode and batched rows.
+MIXED = [("v", 1024, 8192, 32), ("down", 8192, 28672, 32), ("qk", 9216, 8192, 8192)]
+
+
+@pytest.mark.parametrize("name,N,K,G", MIXED)
+def test_mixed_granularity_linears(O, name, N, K, G):
+    log(f"mixed {name}: generate weights {N}x{K} G={G}")
+    W = Weights(O, wl.weights(wl.rng_for("llama70b", 30 + K // 1024 + N // 1024), N, K), G)
+    for M in (16, 256):
+        log(f"mixed {name} M={M}")
+        x = wl.activations(wl.rng_for("llama70b", 31, M * 100 + K // 1024), M, K)
+        rows = sample_rows(M, seed=M + 7, n_random=4) if M > 16 else np.arange(M)
+        _float_case(O, f"mixed {name} M={M}", W, x, rows)
+
+
 @pytest.mark.parametrize("G", [128, 256, 512, 8192])
 def test_granularity_sweep(O, G):
     M, N, K = 4096, 8192, 8192
