@@ -10,6 +10,7 @@ not gfx950 the call raises.
     Y = apex4_w4a4_gemm(A_q, s_a, W_q, s_w, G)          # Y: [M, N] float16
     P = apex4_w4a4_gemm_groupsums(A_q, W_q, G, m0, mr)  # int32 [mr, N, K/G]
     Y = apex4_w4a4_linear(x, W_q, s_w, G)               # quantize + GEMM
+    lin = W4A4Linear(w, G); y = lin(x)                  # drop-in layer (weights quantized once)
 """
 from __future__ import annotations
 
@@ -149,3 +150,41 @@ def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None,
 
 def apex4_version() -> int:
     return int(lib().apex4_version())
+
+
+class W4A4Linear:
+    """Drop-in W4A4 linear layer over the C ABI (APEX4 Sec. 3.2.1, Sec. 4.4):
+    the fp16 weight [N, K] is quantized once with SymQuant (b=4, group G, the
+    same formula as the activations), and every forward quantizes the fp16
+    activations on the fly and runs the W4A4 GEMM (apex4_w4a4_linear).
+
+        lin = W4A4Linear(weight_fp16_cuda, G=128)
+        y = lin(x)             # x [..., K] float16 on the same device -> [..., N]
+
+    The work buffers for the quantized activations are kept and reused while
+    the row count stays the same.  Bias and other dtypes are not supported:
+    the paper's layers are bias-free fp16 linears."""
+
+    def __init__(self, weight, G: int = 128):
+        import torch
+        if weight.dim() != 2:
+            raise ValueError("weight must be [N, K]")
+        self.N, self.K = weight.shape
+        self.G = self.K if G in (0, None) else int(G)
+        self.W_q, self.s_w = apex4_quantize_act(weight.contiguous(), self.G)
+        self._work = None
+        self.device = weight.device
+        self._torch = torch
+
+    def __call__(self, x):
+        lead = x.shape[:-1]
+        if x.shape[-1] != self.K:
+            raise ValueError(f"expected last dimension {self.K}, got {x.shape[-1]}")
+        x2 = x.reshape(-1, self.K).contiguous()
+        M = x2.shape[0]
+        if self._work is None or self._work[0].shape[0] != M:
+            torch = self._torch
+            self._work = (torch.empty((M, self.K // 2), dtype=torch.uint8, device=x2.device),
+                          torch.empty((M, max(self.K // self.G, 1)), dtype=torch.float16, device=x2.device))
+        Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, self._work[0], self._work[1])
+        return Y.reshape(*lead, self.N)
