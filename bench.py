@@ -586,7 +586,9 @@ def gsweep_mode(reps: int = 20):
         del c, Y
 
 
-DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)]
+# (M, N, K): Llama-2-70B o_proj-sized (8192 x 8192), gate/up-sized (28672 x
+# 8192) and down (8192 x 28672) linears at decode batch sizes
+DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)] + [(1, 8192, 28672), (8, 8192, 28672)]
 
 
 def decode_bench(reps: int = 50):
@@ -668,11 +670,16 @@ def decode_bench(reps: int = 50):
         gemm_us = timed(gem)
         lin_g_us = graph_timed(lin, Y)
         gemm_g_us = graph_timed(gem, Y)
+        # the same linear as two kernels (quantizer, then GEMM): what the linear
+        # entry point runs from two rows on, and what its one-row fused kernel replaces
+        two = lambda i: (pk.apex4_quantize_act(x, Gd, Aq, sa), gem(i))
+        two_g_us = graph_timed(two, Y)
         yf = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
         fp16_us = timed(lambda i: torch.matmul(x, fsets[i % len(fsets)].t(), out=yf))
         gbytes = Md * Kd / 2 + Nd * Kd / 2 + 2 * (Md + Nd) * Kd / Gd + 2 * Md * Nd
         out.append({"M": Md, "N": Nd, "K": Kd, "G": Gd, "linear_us": round(lin_us, 2), "gemm_us": round(gemm_us, 2),
                     "linear_graph_us": round(lin_g_us, 2), "gemm_graph_us": round(gemm_g_us, 2),
+                    "quant_then_gemm_graph_us": round(two_g_us, 2),
                     "gemm_hbm_gbs": round(gbytes / (gemm_g_us * 1e-6) / 1e9, 1),
                     "gemm_hbm_frac": round(gbytes / (gemm_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
                     "linear_hbm_gbs": round((gbytes + 2 * Md * Kd) / (lin_g_us * 1e-6) / 1e9, 1),

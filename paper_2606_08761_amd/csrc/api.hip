@@ -145,6 +145,12 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    if (apex4::fused_linear_fits(M, N, K, G)) {
+        const hipError_t e = apex4::launch_linear_fused(static_cast<const uint16_t*>(x), W_q, static_cast<const uint16_t*>(s_w),
+                                                        M, N, K, G, static_cast<uint16_t*>(Y), A_q_work,
+                                                        static_cast<uint16_t*>(s_a_work), st);
+        return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+    }
     hipError_t e = apex4::launch_quantize(static_cast<const uint16_t*>(x), M, K, G, A_q_work,
                                           static_cast<uint16_t*>(s_a_work), st);
     if (e != hipSuccess) return APEX4_ERR_LAUNCH;

@@ -181,6 +181,41 @@ def test_decode_linear(O, N, K):
         assert torch.equal(Y, Y2)
 
 
+# (M, N, K, G) on the linear entry point's fused quantize + GEMM kernel (one
+# row, G in {128, 256, 512}): Llama-2-70B projections, ragged N, and
+# K = 65536 (96 KiB of codes and scales in LDS); the last three take the
+# two-kernel path (K = 122880 does not fit in LDS, two rows, G = K) and check
+# the dispatch around it
+FUSED = [(1, 8192, 8192, 128), (1, 28672, 8192, 128), (1, 8192, 28672, 128), (1, 1024, 8192, 128),
+         (1, 1000, 4096, 256), (1, 520, 8192, 512), (1, 33, 1024, 512), (1, 96, 1536, 128),
+         (1, 300, 65536, 128), (1, 300, 122880, 128), (2, 200, 4096, 128), (1, 64, 4096, 4096)]
+
+
+@pytest.mark.parametrize("M,N,K,G", FUSED)
+def test_fused_linear(O, M, N, K, G):
+    """The linear entry point's one-kernel path: Y and the work buffers equal
+    apex4_quantize_act followed by apex4_w4a4_gemm bit for bit, and Y is within
+    tolerance of the oracle on every row."""
+    import torch
+    m = pk()
+    log(f"fused linear M={M} N={N} K={K} G={G}")
+    w = wl.weights(wl.rng_for("decode", 5, N * 7 + K), N, K)
+    x = wl.activations(wl.rng_for("decode", 6, M * 1000 + K // 128 + G), M, K)
+    Wq_d, sw_d = m.apex4_quantize_act(dev(w), G)
+    Aq_w = torch.full((M, K // 2), 0xAB, dtype=torch.uint8, device="cuda")
+    sa_w = torch.full((M, K // G), float("nan"), dtype=torch.float16, device="cuda")
+    Y = m.apex4_w4a4_linear(dev(x), Wq_d, sw_d, G, A_q_work=Aq_w, s_a_work=sa_w)
+    Aq_d, sa_d = m.apex4_quantize_act(dev(x), G)
+    Y2 = m.apex4_w4a4_gemm(Aq_d, sa_d, Wq_d, sw_d, G)
+    torch.cuda.synchronize()
+    assert torch.equal(Aq_w, Aq_d)
+    assert torch.equal(sa_w.view(torch.int16), sa_d.view(torch.int16))
+    assert torch.equal(Y, Y2)
+    Wq_o, sw_o = O.quantize(w, G)
+    Aq_o, sa_o = O.quantize(x, G)
+    check_tolerance(host(Y), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"fused M={M} N={N} K={K} G={G}")
+
+
 DECODE = [
     (1, 96, 4224, 128), (5, 40, 2560, 512), (32, 300, 1536, 1536), (16, 64, 28672, 256),
     (3, 1000, 1152, 128), (31, 33, 640, 128), (32, 8192, 8192, 512), (8, 520, 8192, 1024),
