@@ -199,12 +199,14 @@ def summarize_mode(args):
                   f"fp16 GEMM (hipBLASLt) {b['fp16_gemm_us']:.1f} us",
                   "", "Decode linears: eager = one Python call per launch (partly launch-bound at these sizes); "
                   "graph = the same calls replayed from a captured graph (GPU time, used for GB/s).", "",
-                  "| decode M | N | K | quantize + GEMM us (eager / graph) | GEMM us (eager / graph) | GEMM HBM GB/s | "
-                  "fp16 GEMM us (eager) | speedup vs fp16 (eager / graph) |",
-                  "|---|---|---|---|---|---|---|---|"]
+                  "Linear = apex4_w4a4_linear from fp16 x (one fused kernel at M=1, quantizer + GEMM otherwise); "
+                  "quantize then GEMM = the two entry points called in turn.", "",
+                  "| decode M | N | K | linear us (eager / graph) | quantize then GEMM us (graph) | GEMM us (eager / graph) | "
+                  "GEMM HBM GB/s | fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
+                  "|---|---|---|---|---|---|---|---|---|"]
         for d in b.get("decode", []):
             lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d['linear_us']} / {d.get('linear_graph_us')} | "
-                         f"{d['gemm_us']} / {d.get('gemm_graph_us')} | {d['gemm_hbm_gbs']} | "
+                         f"{d.get('quant_then_gemm_graph_us')} | {d['gemm_us']} / {d.get('gemm_graph_us')} | {d['gemm_hbm_gbs']} | "
                          f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} / {d.get('speedup_linear_graph_vs_fp16')} |")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
