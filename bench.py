@@ -199,7 +199,7 @@ def summarize_mode(args):
                   f"fp16 GEMM (hipBLASLt) {b['fp16_gemm_us']:.1f} us",
                   "", "Decode linears: eager = one Python call per launch (partly launch-bound at these sizes); "
                   "graph = the same calls replayed from a captured graph (GPU time, used for GB/s).", "",
-                  "Linear = apex4_w4a4_linear from fp16 x (one fused kernel at M=1, quantizer + GEMM otherwise); "
+                  "Linear = apex4_w4a4_linear from fp16 x (one fused kernel at M=1 where it pays, quantizer + GEMM otherwise); "
                   "quantize then GEMM = the two entry points called in turn.", "",
                   "| decode M | N | K | linear us (eager / graph) | quantize then GEMM us (graph) | GEMM us (eager / graph) | "
                   "GEMM HBM GB/s | fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
@@ -673,7 +673,7 @@ def decode_bench(reps: int = 50):
         lin_g_us = graph_timed(lin, Y)
         gemm_g_us = graph_timed(gem, Y)
         # the same linear as two kernels (quantizer, then GEMM): what the linear
-        # entry point runs from two rows on, and what its one-row fused kernel replaces
+        # entry point runs unless its one-row fused kernel pays
         two = lambda i: (pk.apex4_quantize_act(x, Gd, Aq, sa), gem(i))
         two_g_us = graph_timed(two, Y)
         yf = torch.empty((Md, Nd), dtype=torch.float16, device=dev)

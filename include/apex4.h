@@ -107,9 +107,9 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
  * linear layer (Sec. 3.2.1: activations quantized dynamically, weights
  * offline).  Y and the work buffers end up exactly as after
  * apex4_quantize_act(x) into the work buffers followed by apex4_w4a4_gemm on
- * the same stream.  For one row (M = 1) and G in {128, 256, 512} this is one
- * fused kernel that quantizes x in its prologue; otherwise the two kernels
- * are enqueued in that order.
+ * the same stream.  For one row (M = 1) and G in {32, 64, 128, 256, 512}
+ * (G < K) this is one fused kernel that quantizes x in its prologue;
+ * otherwise the two kernels are enqueued in that order.
  *
  *   x [M, K] binary16, W_q [N, K/2], s_w [N, K/G]  (device, read-only);
  *   Y [M, N] binary16 (device, output);

@@ -27,10 +27,17 @@ hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8
                               const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
                               uint16_t* Y, hipStream_t stream);
 
-// Quantize + W4A4 GEMM in one kernel for one row and G in {128, 256, 512}
-// (the activation codes must fit in LDS): Y as launch_quantize followed
-// by launch_gemm gives, bit for bit, and Aq / sa receive the same codes and
-// scales as launch_quantize writes.
+// W4A4 GEMM for one row on the vector ALUs (v_dot8_i32_i4 on the packed
+// codes): weight rows streamed from HBM in 1 KB runs.  gemv_fits() says
+// whether the shape is one it handles.
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G);
+hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream);
+
+// Quantize + W4A4 GEMM in one kernel: the one-row kernel above, quantizing x
+// in its prologue (G in {32, 64, 128, 256, 512}, G < K).  Y as
+// launch_quantize followed by launch_gemm gives, bit for bit, and Aq / sa
+// receive the same codes and scales as launch_quantize writes.
 bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N,
                                int64_t K, int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream);

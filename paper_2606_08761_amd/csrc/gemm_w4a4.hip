@@ -542,6 +542,7 @@ hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P,
                        hipStream_t stream) {
+    if (!P && gemv_fits(M, N, K, G)) return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
     if (!P && decode_fits(M, N, K, G)) return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (big_tiles < device_cu_count()) return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);

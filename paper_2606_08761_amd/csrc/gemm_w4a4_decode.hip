@@ -30,15 +30,10 @@
 //     dequantized with that group's scales.
 //   * The 8 partial fp32 tiles are summed through LDS in a fixed order and
 //     rounded once to binary16.
-//   * Fused linear (FUSE): the kernel takes the binary16 activations instead of
-//     their codes, quantizes them in its prologue (SymQuant, the quantizer's
-//     own arithmetic) into LDS while the first weight stages are in flight, and
-//     reads the codes from LDS.  One kernel launch less per decode step.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include "apex4_internal.h"
-#include "quant_core.h"
 
 namespace apex4 {
 namespace {
@@ -52,8 +47,6 @@ constexpr int COLS = 32;
 constexpr int ROWS = 32;
 constexpr int MAX_SC_LDS = 60 * 1024;         // bytes of each staged scale block ([K/G][32] binary16)
 constexpr int DECODE_PF = 6;                   // stages in flight per wave
-constexpr int FUSE_PAD = 64;                   // bytes after each row of codes in LDS (fused path)
-constexpr int FQ = 8;                          // fused path: 16-byte loads of x in flight per thread
 constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
 constexpr float MAGIC = 12582912.0f;
 
@@ -73,23 +66,14 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
 // are dequantized and reduced.  PF: stages in flight per wave.  GPS: groups per
 // 128-wide stage (1 for G >= 128, 2 for G = 64, 4 for G = 32).  Lane l holds
 // rows 8 (r / 4) + 4 (l / 32) + r % 4 for r < MROWS / 2.
-// FUSE (M <= 8, G in {128, 256, 512}, QL = G / 8): the quantize + GEMM linear
-// in one kernel.  Every workgroup quantizes the binary16 rows x [M, K] itself
-// with the quantizer's arithmetic (quant_core.h, so codes and scales are the
-// same bits), keeps the codes in LDS for the whole kernel (row r at r * FRS
-// bytes), and workgroup 0 also writes codes and scales to aq_out / sa_out.
-// Aq and sa are then unused.
-template <int MROWS, int PF, int GPS, bool FUSE = false, int QL = 16>
+template <int MROWS, int PF, int GPS>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
-    const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
-    const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out) {
+    const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
     constexpr int NR = MROWS / 2;      // output registers per lane that matter
-    static_assert(!FUSE || (MROWS == 8 && GPS == 1), "fused path: up to 8 rows, groups of at least 128");
     __shared__ float red[NWAVE][NR][64];
     // [K/G][32] twice: activation scale of row r and group g at g * 32 + r, then
     // the weight scale of the current tile's column c and group g at g * 32 + c;
-    // with FUSE then the activation codes of rows 0 .. M-1
     extern __shared__ uint16_t sas[];
 
     const int tid = threadIdx.x;
@@ -203,7 +187,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 
     // ring of in-flight stages; (lt, li) is the next (tile, stage) to load.  No
     // load is issued past the last stage.
-    uint4 rw[PF][2], ra[FUSE ? 1 : PF][2];
+    uint4 rw[PF][2], ra[PF][2];
     int lt = 0, li = 0;
     // 32 packed bytes of one lane for a stage: two 16-byte runs (GPS == 1), or
     // four 8-byte pieces 16 apart (one per MFMA) when groups are finer than a stage
@@ -225,7 +209,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const uint8_t* wb = Wq + static_cast<int64_t>(s) * 64;
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
         load32(wb + w_voff, rw[j]);
-        if constexpr (!FUSE) load32(ab + a_voff, ra[j]);
+        load32(ab + a_voff, ra[j]);
         if (++li == per_tile) {
             if (lt + 1 < my_tiles) {
                 li = 0;
@@ -247,89 +231,24 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
         for (int j = 0; j < PF; ++j) load(j);
     }
-    uint8_t* aq_lds = reinterpret_cast<uint8_t*>(sas + 2 * ng * ROWS);
-    const int frs = K / 2 + FUSE_PAD;  // LDS row stride of the codes (padding spreads rows over banks)
-    if constexpr (FUSE) {
-        // SymQuant of rows 0 .. M-1 in slots of 8 values (slot i = row i / (K/8),
-        // values 8 (i % (K/8)) ..), QL consecutive slots per group; slot
-        // base + tid + u NT of round base is lane-consecutive, so each group is
-        // QL neighbouring lanes of one wave, all active.  The first round's
-        // loads go out before the weight-scale staging, each later round's
-        // before the previous round is quantized.
-        const int spr = K / 8;
-        const int nslots = M * spr;
-        uint4 v[FQ];
-        auto load_x = [&](int base) __attribute__((always_inline)) {
-#pragma unroll
-            for (int u = 0; u < FQ; ++u) {
-                const int slot = base + tid + u * NT;
-                v[u] = slot < nslots ? *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(slot) * 8)
-                                     : make_uint4(0u, 0u, 0u, 0u);  // zeros: code 0, scale 0
-            }
-        };
-        load_x(0);
-        if (my_tiles > 0) stage_wscales(0);
-        for (int base = 0; base < nslots; base += FQ * NT) {
-            uint32_t packed[FQ];
-            uint16_t sbits[FQ];
-#pragma unroll
-            for (int u = 0; u < FQ; ++u) {
-                if (base + u * NT < nslots) {  // uniform: thread 0 of the block has a slot
-                    const uint32_t am = quant::group_max<QL>(quant::absmax8_bits(v[u]));
-                    const float sf = quant::scale_of(am, &sbits[u]);
-                    packed[u] = quant::pack8(v[u], sf, quant::inv_of(sf));
-                }
-            }
-            if (base + FQ * NT < nslots) load_x(base + FQ * NT);
-#pragma unroll
-            for (int u = 0; u < FQ; ++u) {
-                const int slot = base + tid + u * NT;
-                if (slot < nslots) {
-                    const int r = slot / spr, c = slot - r * spr;
-                    *reinterpret_cast<uint32_t*>(aq_lds + r * frs + 4 * c) = packed[u];
-                    const bool lead = (c & (QL - 1)) == 0;
-                    if (lead) sas[(c / QL) * ROWS + r] = sbits[u];
-                    if (blockIdx.x == 0) {
-                        reinterpret_cast<uint32_t*>(aq_out)[slot] = packed[u];
-                        if (lead) sa_out[slot / QL] = sbits[u];
-                    }
-                }
-            }
-        }
-        // rows M .. 31 of the activation scales: any finite value (those rows'
-        // outputs are never stored)
-        for (int i = tid; i < ng * ROWS; i += NT)
-            if ((i & (ROWS - 1)) >= M) sas[i] = 0;
-    } else {
-        // activation scales of rows 0 .. 31 (rows past M clamped) and the first
-        // tile's weight scales, their loads in flight together
-        const int c0 = tile_col0(0);
-        if (my_tiles > 0) stage(sa, M - 1, sas, sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
-        else stage(sa, M - 1, sas, nullptr, 0, nullptr);
-    }
+    // activation scales of rows 0 .. 31 (rows past M clamped) and the first
+    // tile's weight scales, their loads in flight together
+    const int c0 = tile_col0(0);
+    if (my_tiles > 0) stage(sa, M - 1, sas, sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
+    else stage(sa, M - 1, sas, nullptr, 0, nullptr);
     if (pf_sc && my_tiles > 1) prefetch_wscales(1);
     __syncthreads();  // activation scales and the first tile's weight scales staged
 
-    const int a_lds_off = min(l32, M - 1) * frs + 32 * lh;  // FUSE: this lane's code row in LDS
     int pi = 0;  // stage-in-tile of the next processed stage
     auto process = [&](int j) {
         const int s_raw = wave + NWAVE * pi;
         const bool live = s_raw < nks;
         const int s = min(s_raw, nks - 1);
         i32x4 bw[4], af[4];
-        uint4 ua[2];
-        if constexpr (FUSE) {
-            const uint8_t* ap = aq_lds + a_lds_off + s * 64;
-            ua[0] = *reinterpret_cast<const uint4*>(ap);
-            ua[1] = *reinterpret_cast<const uint4*>(ap + 16);
-        } else {
-            ua[0] = ra[j][0];
-            ua[1] = ra[j][1];
-        }
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             const uint4& v = rw[j][kk >> 1];
-            const uint4& u = ua[kk >> 1];
+            const uint4& u = ra[j][kk >> 1];
             bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             af[kk] = (kk & 1) ? frag2(u.z, u.w) : frag2(u.x, u.y);
         }
@@ -418,40 +337,12 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
     const size_t lds = 2 * static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
-    const uint16_t* no_x = nullptr;
-    uint8_t* no_aq = nullptr;
-    uint16_t* no_sa = nullptr;
     if (M <= 8)
-        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y, no_x, no_aq, no_sa);
+        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
     else if (M <= 16)
-        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y, no_x, no_aq, no_sa);
+        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
     else
-        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y, no_x, no_aq, no_sa);
-    return hipGetLastError();
-}
-
-// LDS of the fused kernel: both scale blocks, then M rows of codes
-size_t fused_lds_bytes(int64_t M, int64_t K, int64_t G) {
-    return 2 * static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t) + static_cast<size_t>(M) * (K / 2 + FUSE_PAD);
-}
-constexpr size_t FUSED_LDS_MAX = 160 * 1024 - sizeof(float) * NWAVE * 4 * 64;  // all LDS but the reduction buffer
-
-template <int QL>
-hipError_t launch_fused_ql(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N, int64_t K,
-                           int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream) {
-    static bool lds_attr_set = false;  // benign race: every caller sets the same value
-    if (!lds_attr_set) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(w4a4_decode_kernel<8, DECODE_PF, 1, true, QL>),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(FUSED_LDS_MAX));
-        if (e != hipSuccess) return e;
-        lds_attr_set = true;
-    }
-    const int64_t tiles = (N + COLS - 1) / COLS;
-    const int64_t grid = tiles < device_cu_count() ? tiles : device_cu_count();
-    const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
-    hipLaunchKernelGGL((w4a4_decode_kernel<8, DECODE_PF, 1, true, QL>), gd, bd, fused_lds_bytes(M, K, G), stream,
-                       static_cast<const uint8_t*>(nullptr), static_cast<const uint16_t*>(nullptr), Wq, sw,
-                       static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, x, Aq, sa);
+        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
     return hipGetLastError();
 }
 
@@ -473,23 +364,6 @@ int device_cu_count() {
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
     const bool g_ok = G == K || G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024;
     return M >= 1 && M <= ROWS && N >= 1 && g_ok && (K / G) * ROWS * 2 <= MAX_SC_LDS;
-}
-
-// Every workgroup quantizes all M rows, so the prologue grows with M while the
-// separate quantizer costs about the same at any small M: one row (single-token
-// decode) is where the fused kernel measured faster (0.8 - 2.5 us on MI355X for
-// N = 1024 .. 28672, K = 8192 .. 28672), from two rows on the two kernels win or
-// tie.  The kernel itself handles up to 8 rows.
-bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
-    return M == 1 && N >= 1 && (G == 128 || G == 256 || G == 512) && G < K && fused_lds_bytes(M, K, G) <= FUSED_LDS_MAX;
-}
-
-hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N, int64_t K,
-                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream) {
-    if (!fused_linear_fits(M, N, K, G)) return hipErrorInvalidValue;
-    if (G == 128) return launch_fused_ql<16>(x, Wq, sw, M, N, K, G, Y, Aq, sa, stream);
-    if (G == 256) return launch_fused_ql<32>(x, Wq, sw, M, N, K, G, Y, Aq, sa, stream);
-    return launch_fused_ql<64>(x, Wq, sw, M, N, K, G, Y, Aq, sa, stream);
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,

@@ -1,0 +1,247 @@
+// W4A4 group GEMM for a single activation row (single-token decode) on gfx950,
+// on the vector ALUs instead of the matrix cores.
+//
+// Same result as the tiled kernel (APEX4 Sec. 3.2.1, Eq. group_decomposition):
+// Y[0, n] = sum_g s_a[g] s_w[n, g] sum_{k in g} A_q[k] W_q[n, k].  At one row
+// the work is a matrix-vector product bound by streaming W from HBM, so the
+// design is about the load stream, not the contraction:
+//   * v_dot8_i32_i4 multiplies 8 packed signed nibbles of A with the 8 nibbles
+//     of W at the same k and adds the products: the packed codes are used as
+//     stored, with no unpacking.
+//   * A wave streams whole weight rows.  One load instruction covers 1 KB of
+//     one row (64 lanes x 16 bytes, contiguous), so lane l of chunk c holds the
+//     32 codes k in [2048 c + 32 l, 2048 c + 32 l + 32), all in one group
+//     (every supported G is a multiple of 32).  Each wave keeps its whole share
+//     of rows (up to 16 loads per lane) in flight at once, and the workgroups
+//     are small (4 waves) so that many waves per CU keep the HBM queue full.
+//   * The lane's 32-code partial sum is exact in int32 (|p| <= 2048).  It is
+//     dequantized right away with its group's scales, t = p s_a, acc += t s_w
+//     (binary32; splitting a group into 32-code partials changes only the fp32
+//     rounding, never the exact group sum).
+//   * A's codes and scales (as binary32) sit in LDS, staged once per
+//     workgroup while the first weight loads are in flight; every wave reads
+//     the 16 bytes matching its weight load.
+//   * A row's 64 lane partials are summed in a fixed butterfly order and
+//     rounded once to binary16.
+//   * Fused linear (FUSE, G <= 512): the kernel takes the binary16 row x
+//     instead of its codes and quantizes it into LDS in the prologue with the
+//     quantizer's own arithmetic (quant_core.h: same codes and scales, bit for
+//     bit); workgroup 0 also writes them to the caller's work buffers.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include "apex4_internal.h"
+#include "quant_core.h"
+
+namespace apex4 {
+namespace {
+
+constexpr int GV_WAVES = 4;     // waves per workgroup
+constexpr int GV_NT = 64 * GV_WAVES;
+constexpr int GV_LOADS = 16;    // 16-byte weight loads in flight per lane
+constexpr int GV_CHUNK = 1024;  // bytes of a weight row per load instruction
+constexpr int GV_FQ = 4;        // fused prologue: 16-byte loads of x in flight per thread
+constexpr int GV_MAX_LDS = 64 * 1024;
+
+__device__ __forceinline__ float gv_h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+
+// Sum over the 64 lanes of a wave in a fixed order (every lane gets the sum).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// Wave w of workgroup b owns weight rows n0 .. n0 + rpw - 1,
+// n0 = (b * GV_WAVES + w) * rpw, and walks its (row, chunk) pairs row-major in
+// batches of GV_LOADS loads.  lgG: log2(G), or 31 for G = K (one group).
+// QL = G / 8: slots of 8 values per group (FUSE only).
+template <bool FUSE, int QL>
+__global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
+    const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
+    const uint16_t* __restrict__ sw, int N, int K, int G, int lgG, int rpw, uint16_t* __restrict__ Y,
+    const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out) {
+    // A's codes (K/2 bytes), then s_a as binary32 [K/G]
+    extern __shared__ uint4 gv_lds[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kb = K / 2;                            // bytes per row
+    const int nch = (kb + GV_CHUNK - 1) / GV_CHUNK;  // chunks per row
+    const int ng = K / G;
+    const int n0 = (static_cast<int>(blockIdx.x) * GV_WAVES + wave) * rpw;
+    const int units = rpw * nch;
+    float* sa_lds = reinterpret_cast<float*>(gv_lds + kb / 16);
+
+    uint4 w[GV_LOADS];
+    uint16_t sws[GV_LOADS];
+    // loads of pairs f0 .. f0 + GV_LOADS - 1 (pairs past the wave's share, rows
+    // past N and bytes past the row end load nothing)
+    auto issue = [&](int f0) __attribute__((always_inline)) {
+        int r = f0 / nch, c = f0 - r * nch;
+#pragma unroll
+        for (int j = 0; j < GV_LOADS; ++j) {
+            const int n = n0 + r;
+            const int off = c * GV_CHUNK + 16 * lane;
+            const bool ok = f0 + j < units && n < N && off < kb;
+            w[j] = ok ? *reinterpret_cast<const uint4*>(Wq + static_cast<int64_t>(n) * kb + off) : make_uint4(0u, 0u, 0u, 0u);
+            sws[j] = ok ? sw[static_cast<int64_t>(n) * ng + ((2 * off) >> lgG)] : static_cast<uint16_t>(0);
+            if (++c == nch) {
+                c = 0;
+                ++r;
+            }
+        }
+    };
+
+    if (n0 < N) issue(0);
+    // A's codes and scales into LDS while the first weight loads are in flight
+    if constexpr (FUSE) {
+        // SymQuant of x in slots of 8 values (slot s: k in [8 s, 8 s + 8)),
+        // QL consecutive slots per group.  Slot base + tid + u GV_NT is
+        // lane-consecutive, so a group is QL neighbouring lanes of one wave,
+        // all active (slots past K load zeros: code 0, scale 0).
+        const int nslots = K / 8;
+        uint4 v[GV_FQ];
+        auto load_x = [&](int base) __attribute__((always_inline)) {
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                const int s = base + tid + u * GV_NT;
+                v[u] = s < nslots ? *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(s) * 8) : make_uint4(0u, 0u, 0u, 0u);
+            }
+        };
+        load_x(0);
+        for (int base = 0; base < nslots; base += GV_FQ * GV_NT) {
+            uint32_t packed[GV_FQ];
+            uint16_t sbits[GV_FQ];
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                if (base + u * GV_NT < nslots) {  // uniform: thread 0 has a slot
+                    const uint32_t am = quant::group_max<QL>(quant::absmax8_bits(v[u]));
+                    const float sf = quant::scale_of(am, &sbits[u]);
+                    packed[u] = quant::pack8(v[u], sf, quant::inv_of(sf));
+                }
+            }
+            if (base + GV_FQ * GV_NT < nslots) load_x(base + GV_FQ * GV_NT);
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                const int s = base + tid + u * GV_NT;
+                if (s < nslots) {
+                    reinterpret_cast<uint32_t*>(gv_lds)[s] = packed[u];
+                    const bool lead = (s & (QL - 1)) == 0;
+                    if (lead) sa_lds[s / QL] = gv_h2f(sbits[u]);
+                    if (blockIdx.x == 0) {
+                        reinterpret_cast<uint32_t*>(aq_out)[s] = packed[u];
+                        if (lead) sa_out[s / QL] = sbits[u];
+                    }
+                }
+            }
+        }
+    } else {
+        for (int i = tid; i < kb / 16; i += GV_NT) gv_lds[i] = reinterpret_cast<const uint4*>(Aq)[i];
+        for (int i = tid; i < ng; i += GV_NT) sa_lds[i] = gv_h2f(sa[i]);
+    }
+    __syncthreads();
+    if (n0 >= N) return;  // after the only barrier
+
+    float acc = 0.f;
+    for (int f0 = 0; f0 < units; f0 += GV_LOADS) {
+        if (f0 > 0) issue(f0);
+        int r = f0 / nch, c = f0 - r * nch;
+#pragma unroll
+        for (int j = 0; j < GV_LOADS; ++j) {
+            if (f0 + j < units) {  // uniform
+                const int off = c * GV_CHUNK + 16 * lane;
+                if (off < kb) {
+                    const uint4 a = gv_lds[off >> 4];
+                    int p = __builtin_amdgcn_sdot8(static_cast<int>(a.x), static_cast<int>(w[j].x), 0, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.y), static_cast<int>(w[j].y), p, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.z), static_cast<int>(w[j].z), p, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.w), static_cast<int>(w[j].w), p, false);
+                    const float t = static_cast<float>(p) * sa_lds[(2 * off) >> lgG];
+                    acc = fmaf(t, gv_h2f(sws[j]), acc);
+                }
+                if (c == nch - 1) {  // row n0 + r complete (uniform)
+                    const float s = wave_sum(acc);
+                    const int n = n0 + r;
+                    if (lane == 0 && n < N) Y[n] = __half_as_ushort(__float2half_rn(s));
+                    acc = 0.f;
+                }
+            }
+            if (++c == nch) {
+                c = 0;
+                ++r;
+            }
+        }
+    }
+}
+
+size_t gemv_lds_bytes(int64_t K, int64_t G) { return static_cast<size_t>(K / 2) + 4 * static_cast<size_t>(K / G); }
+
+// Rows per wave and workgroups: fill the load batch, but keep at least 8 waves
+// per CU when N allows.
+struct GemvGrid {
+    int64_t rpw, grid;
+};
+GemvGrid gemv_grid(int64_t N, int64_t K) {
+    const int64_t nch = (K / 2 + GV_CHUNK - 1) / GV_CHUNK;
+    int64_t rpw = GV_LOADS / nch;
+    const int64_t spread = N / (8 * static_cast<int64_t>(device_cu_count()));
+    if (rpw > spread) rpw = spread;
+    if (rpw < 1) rpw = 1;
+    const int64_t waves = (N + rpw - 1) / rpw;
+    return {rpw, (waves + GV_WAVES - 1) / GV_WAVES};
+}
+
+template <bool FUSE, int QL>
+hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t N,
+                         int64_t K, int64_t G, uint16_t* Y, const uint16_t* x, uint8_t* aq_out, uint16_t* sa_out,
+                         hipStream_t stream) {
+    const GemvGrid gg = gemv_grid(N, K);
+    int lgG = 31;
+    if (G != K)
+        for (lgG = 5; (int64_t{1} << lgG) < G; ++lgG) {
+        }
+    hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL>), dim3(static_cast<unsigned>(gg.grid)), dim3(GV_NT),
+                       gemv_lds_bytes(K, G), stream, Aq, sa, Wq, sw, static_cast<int>(N), static_cast<int>(K),
+                       static_cast<int>(G), lgG, static_cast<int>(gg.rpw), Y, x, aq_out, sa_out);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+    const bool g_ok = G == K || G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024;
+    return M == 1 && N >= 1 && g_ok && gemv_lds_bytes(K, G) <= GV_MAX_LDS;
+}
+
+hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+    if (!gemv_fits(M, N, K, G)) return hipErrorInvalidValue;
+    return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, stream);
+}
+
+// Every workgroup quantizes all of x, so the fused prologue's total work is
+// (workgroups x K): up to 2^23 it is cheaper than a second launch (measured on
+// MI355X: 0.8 - 1.4 us faster at N = 1024 .. 10240, K = 8192), beyond it the
+// separate quantizer wins (0.9 us at N = 28672, 12 us at N = 8192, K = 28672).
+constexpr int64_t GV_FUSE_WORK = int64_t{1} << 23;
+
+bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+    return gemv_fits(M, N, K, G) && (G == 32 || G == 64 || G == 128 || G == 256 || G == 512) && G < K &&
+           gemv_grid(N, K).grid * K <= GV_FUSE_WORK;
+}
+
+hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N, int64_t K,
+                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream) {
+    if (!fused_linear_fits(M, N, K, G)) return hipErrorInvalidValue;
+    const uint8_t* no_aq = nullptr;
+    const uint16_t* no_sa = nullptr;
+    switch (G) {
+        case 32: return launch_gemv_t<true, 4>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+        case 64: return launch_gemv_t<true, 8>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+        case 128: return launch_gemv_t<true, 16>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+        case 256: return launch_gemv_t<true, 32>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+        default: return launch_gemv_t<true, 64>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+    }
+}
+
+}  // namespace apex4

@@ -181,14 +181,17 @@ def test_decode_linear(O, N, K):
         assert torch.equal(Y, Y2)
 
 
-# (M, N, K, G) on the linear entry point's fused quantize + GEMM kernel (one
-# row, G in {128, 256, 512}): Llama-2-70B projections, ragged N, and
-# K = 65536 (96 KiB of codes and scales in LDS); the last three take the
-# two-kernel path (K = 122880 does not fit in LDS, two rows, G = K) and check
-# the dispatch around it
-FUSED = [(1, 8192, 8192, 128), (1, 28672, 8192, 128), (1, 8192, 28672, 128), (1, 1024, 8192, 128),
-         (1, 1000, 4096, 256), (1, 520, 8192, 512), (1, 33, 1024, 512), (1, 96, 1536, 128),
-         (1, 300, 65536, 128), (1, 300, 122880, 128), (2, 200, 4096, 128), (1, 64, 4096, 4096)]
+# (M, N, K, G) of the linear entry point at one row.  The fused quantize + GEMM
+# kernel (G in {32, 64, 128, 256, 512}, G < K, when its redundant prologue work
+# is small) takes: Llama-2-70B o_proj and v_proj sizes, ragged N, a partial
+# last 1 KB chunk (K = 1536), every fused G, and K = 122880, the largest whose
+# codes and scales fit the kernel's 64 KiB of LDS.  The rest take the two
+# kernels: larger N x K (gate/up, down), K = 131072 (does not fit), two rows,
+# G = K and G = 1024.  Either way the result must equal quantize-then-GEMM.
+FUSED = [(1, 8192, 8192, 128), (1, 1024, 8192, 128), (1, 1000, 4096, 256), (1, 520, 8192, 512),
+         (1, 33, 1024, 512), (1, 96, 1536, 128), (1, 1024, 8192, 32), (1, 520, 4096, 64), (1, 200, 122880, 128),
+         (1, 28672, 8192, 128), (1, 8192, 28672, 128), (1, 200, 131072, 128), (2, 200, 4096, 128),
+         (1, 64, 4096, 4096), (1, 72, 8192, 1024)]
 
 
 @pytest.mark.parametrize("M,N,K,G", FUSED)
@@ -223,12 +226,17 @@ DECODE = [
     # G = 32 and 64 on the streaming kernel: the mixed configuration's value
     # (N=1024, K=8192) and down (K=28672) projections at decode batch sizes
     (16, 1024, 8192, 32), (16, 2048, 28672, 32), (1, 520, 4096, 64), (9, 96, 8192, 32), (32, 64, 2048, 64),
+    # one row (the dot-product kernel): every G, G = K not a power of two,
+    # partial last chunks (K/2 not a multiple of 1 KB), N below one wave's share
+    (1, 1000, 8192, 32), (1, 257, 2048, 1024), (1, 300, 3072, 3072), (1, 8192, 28672, 128),
+    (1, 3, 640, 128), (1, 4097, 8192, 256), (1, 100, 122880, 512),
 ]
 
 
 @pytest.mark.parametrize("M,N,K,G", DECODE)
 def test_decode_kernel_shapes(O, M, N, K, G):
-    """Up to 32 rows run on the weight-streaming kernel (K split over 8 waves)."""
+    """Up to 32 rows run on the weight-streaming kernel (K split over 8 waves),
+    one row on the dot-product kernel."""
     log(f"decode kernel M={M} N={N} K={K} G={G}")
     r = np.random.default_rng(M * 104729 + N * 13 + K + G)
     Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
