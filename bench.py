@@ -85,14 +85,17 @@ def traffic_from_profile():
         return None
 
 
-def cpu_baseline(target_s: float):
+def cpu_baseline(target_s: float, threads: int = 0):
     """The oracle (quantize the sampled activation rows + binary64 GEMM rows)
-    timed on this host for a bounded row sample; TOPS scaled to 2 * rows * N * K."""
+    timed on this host for a bounded row sample; TOPS scaled to 2 * rows * N * K.
+    threads > 0 pins the oracle's OpenMP thread count (default: all)."""
     from oracle import oracle as O
     from paper_2606_08761_amd import workloads as wl
 
     x, w = wl.float_workload("paper", M, N, K)
     Wq, sw = O.quantize(w, G)                       # weights are quantized offline
+    if threads > 0:
+        O.set_num_threads(threads)
     rows = 2
     while True:
         t0 = time.perf_counter()
@@ -238,8 +241,10 @@ def layers_mode(reps: int = 10):
     """The linears of one Llama-2-70B decoder layer under the uniform G=128 and the
     mixed configuration, each linear timed as quantize + W4A4 GEMM from fp16
     activations (apex4_w4a4_linear), next to fp16 GEMMs of the same shapes
-    (torch.matmul -> hipBLASLt).  Weights are rotated over copies larger than the
-    Infinity Cache; codes and scales are random (speed does not depend on values)."""
+    (torch.matmul -> hipBLASLt).  Weights are rotated over at least 512 MB of
+    copies (twice the Infinity Cache); codes and scales are random (speed does
+    not depend on values).  The W4A4 linears are timed from a replayed graph of
+    `reps` calls (GPU time, no Python launch overhead), the fp16 GEMMs eagerly."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import workloads as wl
@@ -259,15 +264,38 @@ def layers_mode(reps: int = 10):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n * 1e3
 
+    def graph_timed(fn, n):
+        fn(0)
+        torch.cuda.synchronize()
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for i in range(n):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        del g
+        return e0.elapsed_time(e1) / n * 1e3
+
+    def copies(nbytes):
+        return max(2, -(-ROTATE_BYTES // nbytes))
+
     for cfg, linears in LAYER_CONFIGS.items():
         wsets = {}
         for name, Nl, Kl, Gl in linears:
             Gv = Gl or Kl
             Wq = torch.from_numpy(wl.random_codes(r, Nl, Kl)).to(dev)
             sw = torch.from_numpy(wl.random_scales(r, Nl, Kl // Gv)).to(dev)
-            wsets[name] = [(Wq, sw)] + [(Wq.clone(), sw.clone()) for _ in range(1)]
+            R = copies(Nl * Kl // 2 + 2 * Nl * (Kl // Gv))
+            wsets[name] = [(Wq, sw)] + [(Wq.clone(), sw.clone()) for _ in range(R - 1)]
         for Ml in LAYER_M:
-            per = {}
+            per, gbs = {}, {}
             for name, Nl, Kl, Gl in linears:
                 Gv = Gl or Kl
                 x = torch.from_numpy(wl.activations(wl.rng_for("llama70b", 98, Ml + Kl), Ml, Kl)).to(dev)
@@ -275,22 +303,28 @@ def layers_mode(reps: int = 10):
                 Aq = torch.empty((Ml, Kl // 2), dtype=torch.uint8, device=dev)
                 sa = torch.empty((Ml, Kl // Gv), dtype=torch.float16, device=dev)
                 ws = wsets[name]
-                per[name] = round(timed(lambda i: pk.apex4_w4a4_linear(x, ws[i % 2][0], ws[i % 2][1], Gv, Y, Aq, sa),
-                                        reps), 2)
+                t = graph_timed(lambda i: pk.apex4_w4a4_linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa),
+                                reps)
+                per[name] = round(t, 2)
+                # algorithmic HBM bytes of the linear: x, codes, scales, Y
+                nbytes = 2 * Ml * Kl + Ml * Kl / 2 + Nl * Kl / 2 + 2 * (Ml + Nl) * Kl / Gv + 2 * Ml * Nl
+                gbs[name] = round(nbytes / (t * 1e-6) / 1e9)
                 del x, Y, Aq, sa
-            print(json.dumps({"mode": "layers", "config": cfg, "M": Ml, "linear_us": per,
+            print(json.dumps({"mode": "layers", "config": cfg, "M": Ml, "linear_us": per, "hbm_gbs": gbs,
                               "total_us": round(sum(per.values()), 2)}), flush=True)
         del wsets
         torch.cuda.empty_cache()
     # fp16 GEMMs of the same shapes (the value projection is part of qkv)
     shapes = [("qkv", 10240, 8192), ("o", 8192, 8192), ("gate_up", 57344, 8192), ("down", 8192, 28672)]
-    wf = {n: [torch.randn(Nl, Kl, dtype=torch.float16, device=dev) * 0.02 for _ in range(2)] for n, Nl, Kl in shapes}
     for Ml in LAYER_M:
         per = {}
         for name, Nl, Kl in shapes:
+            wf = [torch.randn(Nl, Kl, dtype=torch.float16, device=dev) * 0.02 for _ in range(copies(2 * Nl * Kl))]
             x = torch.randn(Ml, Kl, dtype=torch.float16, device=dev)
             Y = torch.empty((Ml, Nl), dtype=torch.float16, device=dev)
-            per[name] = round(timed(lambda i: torch.matmul(x, wf[name][i % 2].t(), out=Y), reps), 2)
+            per[name] = round(timed(lambda i: torch.matmul(x, wf[i % len(wf)].t(), out=Y), reps), 2)
+            del wf, x, Y
+            torch.cuda.empty_cache()
         print(json.dumps({"mode": "layers", "config": "fp16", "M": Ml, "linear_us": per,
                           "total_us": round(sum(per.values()), 2)}), flush=True)
 
@@ -301,8 +335,9 @@ def summarize_layers(path, command):
     tot = {(r["config"], r["M"]): r for r in rows}
     lines = ["# Llama-2-70B decoder-layer linears: uniform G=128 vs mixed granularity vs fp16", "",
              "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
-             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear), "
-             "weights rotated over 2 copies; fp16 is torch.matmul (hipBLASLt) on the same shapes. "
+             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear) "
+             "from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
+             "torch.matmul (hipBLASLt) on the same shapes, rotated the same way, timed eagerly. "
              "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
              "share one per-channel GEMM (N=9216).", "",
              "| M | g128 us | mix us | fp16 us | g128 speedup vs fp16 | mix speedup vs fp16 |",
@@ -313,9 +348,12 @@ def summarize_layers(path, command):
             continue
         lines.append(f"| {Ml} | {g['total_us']} | {mx['total_us']} | {f['total_us']} | "
                      f"{f['total_us'] / g['total_us']:.2f} | {f['total_us'] / mx['total_us']:.2f} |")
-    lines += ["", "Per linear (us):", "", "| config | M | per linear |", "|---|---|---|"]
+    lines += ["", "Per linear (us; W4A4 rows also give the algorithmic HBM GB/s of x, codes, scales and Y):", "",
+              "| config | M | per linear |", "|---|---|---|"]
     for r in rows:
-        lines.append(f"| {r['config']} | {r['M']} | " + ", ".join(f"{k} {v}" for k, v in r["linear_us"].items()) + " |")
+        g = r.get("hbm_gbs", {})
+        lines.append(f"| {r['config']} | {r['M']} | " +
+                     ", ".join(f"{k} {v}" + (f" ({g[k]} GB/s)" if k in g else "") for k, v in r["linear_us"].items()) + " |")
     with open(os.path.join(ROOT, "profiles", "layer_sweep_llama2_70b.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -765,7 +803,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     quant_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    gemm_all = [e[1].elapsed_time(e[2]) for e in evs]
+    gemm_ms = float(np.mean(gemm_all))
     ms_per_step = wall * 1e3 / args.steps
     ops = 2.0 * M * N * K
     value = ops / (ms_per_step * 1e-3) / 1e12
@@ -831,6 +870,7 @@ def main():
         "quant_us": round(quant_ms * 1e3, 3),
         "quant_hbm_gbs": round((2.5 * M * K + 2 * M * K / G) / (quant_ms * 1e-3) / 1e9, 1),
         "gemm_us": round(gemm_ms * 1e3, 3),
+        "gemm_us_p10_p50_p90": [round(float(np.percentile(gemm_all, q)) * 1e3, 3) for q in (10, 50, 90)],
         "gemm_tops": round(gemm_tops, 2),
         "gemm_pct_int8_peak": round(100 * gemm_tops / INT8_PEAK_TOPS, 2),
         "gemm_random_codes_us": round(codes_gemm_ms * 1e3, 3),
@@ -843,6 +883,8 @@ def main():
         line["decode"] = decode_bench()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+        # the same oracle on one host thread (a shorter sample)
+        line["cpu_baseline_1thread"] = cpu_baseline(args.cpu_seconds / 2, threads=1)
     print(json.dumps(line), flush=True)
 
 

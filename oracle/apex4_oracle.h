@@ -64,6 +64,8 @@ int apex4o_gemm_rows(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
 
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int apex4o_num_threads(void);
+/* Threads used by the following oracle calls (OpenMP; n > 0).  Timing only. */
+void apex4o_set_num_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -50,6 +50,8 @@ def _load():
     lib.apex4o_gemm_rows.restype = ctypes.c_int
     lib.apex4o_num_threads.argtypes = []
     lib.apex4o_num_threads.restype = ctypes.c_int
+    lib.apex4o_set_num_threads.argtypes = [ctypes.c_int]
+    lib.apex4o_set_num_threads.restype = None
     _lib = lib
     return lib
 
@@ -131,3 +133,8 @@ def gemm_f16(Aq, sa, Wq, sw, K: int, G: int, rows=None):
 
 def num_threads() -> int:
     return int(_load().apex4o_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the following oracle calls (timing only; results do not depend on it)."""
+    _load().apex4o_set_num_threads(int(n))

@@ -112,7 +112,7 @@ __device__ __forceinline__ i32x16 splat16(int v) {
 
 // One workgroup computes a BM x BN tile with WAVES_M x WAVES_N waves; each
 // wave owns MI x NJ blocks of 32 x 32 (rows x columns).
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS>
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
@@ -202,44 +202,49 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + (FINE ? 8 : 32) * lh;
     }
 
-    uint4 ra[A_CH];
-    uint16_t rsc[GPS] = {};
-    auto load_a = [&](int ks) {
+    // Global loads run PF stages ahead: stage s lives in register slot s % PF
+    // (activations and their scales until stored to LDS, weights until widened).
+    uint4 ra[PF][A_CH];
+    uint16_t rsc[PF][GPS] = {};
+    auto load_a = [&](int ks, auto SLOT) __attribute__((always_inline)) {
+        constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Aq + static_cast<int64_t>(ks) * (KS / 2);
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
+        for (int i = 0; i < A_CH; ++i) ra[sl][i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
         if constexpr (MODE != kDump) {
             // the GPS groups of a stage are adjacent in a scale row (K / G is a multiple of GPS)
             const uint16_t* sp = sc_base + sc_off + static_cast<uint32_t>(ks / spg) * GPS;
             if constexpr (GPS == 1) {
-                rsc[0] = *sp;
+                rsc[sl][0] = *sp;
             } else if constexpr (GPS == 2) {
                 const uint32_t v = *reinterpret_cast<const uint32_t*>(sp);
-                rsc[0] = static_cast<uint16_t>(v);
-                rsc[1] = static_cast<uint16_t>(v >> 16);
+                rsc[sl][0] = static_cast<uint16_t>(v);
+                rsc[sl][1] = static_cast<uint16_t>(v >> 16);
             } else {
                 const uint2 v = *reinterpret_cast<const uint2*>(sp);
-                rsc[0] = static_cast<uint16_t>(v.x);
-                rsc[1] = static_cast<uint16_t>(v.x >> 16);
-                rsc[2] = static_cast<uint16_t>(v.y);
-                rsc[3] = static_cast<uint16_t>(v.y >> 16);
+                rsc[sl][0] = static_cast<uint16_t>(v.x);
+                rsc[sl][1] = static_cast<uint16_t>(v.x >> 16);
+                rsc[sl][2] = static_cast<uint16_t>(v.y);
+                rsc[sl][3] = static_cast<uint16_t>(v.y >> 16);
             }
         }
     };
-    auto store_a = [&](int buf) {
+    auto store_a = [&](int buf, auto SLOT) __attribute__((always_inline)) {
+        constexpr int sl = decltype(SLOT)::value;
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
-            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0[i]]) = frag2(ra[i].x, ra[i].y);
-            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1[i]]) = frag2(ra[i].z, ra[i].w);
+            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0[i]]) = frag2(ra[sl][i].x, ra[sl][i].y);
+            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1[i]]) = frag2(ra[sl][i].z, ra[sl][i].w);
         }
         if constexpr (MODE != kDump) {
 #pragma unroll
-            for (int gi = 0; gi < GPS; ++gi) st[buf].scale[gi][tid] = rsc[gi];
+            for (int gi = 0; gi < GPS; ++gi) st[buf].scale[gi][tid] = rsc[sl][gi];
         }
     };
-    // w[j][kk / 2] holds the two packed dwords of MFMA kk (x, y for even kk, z, w for odd)
-    uint4 w[NJ][2];
-    auto load_w = [&](int ks) {
+    // w[slot][j][kk / 2] holds the two packed dwords of MFMA kk (x, y for even kk, z, w for odd)
+    uint4 w[PF][NJ][2];
+    auto load_w = [&](int ks, auto SLOT) __attribute__((always_inline)) {
+        constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2);
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -249,11 +254,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
                 const uint2 q1 = *reinterpret_cast<const uint2*>(base + w_off[j] + 16);
                 const uint2 q2 = *reinterpret_cast<const uint2*>(base + w_off[j] + 32);
                 const uint2 q3 = *reinterpret_cast<const uint2*>(base + w_off[j] + 48);
-                w[j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
-                w[j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+                w[sl][j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+                w[sl][j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
             } else {
-                w[j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
-                w[j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
+                w[sl][j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
+                w[sl][j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
             }
         }
     };
@@ -304,19 +309,20 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
 
     // One K stage: widen this wave's weight fragments, issue the next stage's
     // weight loads into the freed registers, then run the row blocks.
-    auto compute = [&](int buf, int next, auto FIRST) {
+    auto compute = [&](int buf, int next, auto FIRST, auto SLOT) __attribute__((always_inline)) {
         constexpr bool group_first = decltype(FIRST)::value;
+        constexpr int sl = decltype(SLOT)::value;
         i32x4 bw[NJ][KK];
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-                const uint4& v = w[j][kk >> 1];
+                const uint4& v = w[sl][j][kk >> 1];
                 bw[j][kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             }
         // keep both weight copies from being live at once (register budget)
         __builtin_amdgcn_sched_barrier(0);
-        load_w(next);
+        load_w(next, SLOT);
         __builtin_amdgcn_sched_barrier(0);
         uint2 swh[ROTATE ? NJ : 1][4];
         float sav[ROTATE ? MI : 1];
@@ -358,17 +364,18 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
 
     // One K stage holding GPS whole groups (G < 128): for each group and row
     // block, KPG MFMAs from the bias, then dequantize (or dump) right away.
-    auto compute_fine = [&](int buf, int next, int ks) __attribute__((always_inline)) {
+    auto compute_fine = [&](int buf, int next, int ks, auto SLOT) __attribute__((always_inline)) {
+        constexpr int sl = decltype(SLOT)::value;
         i32x4 bw[NJ][KK];
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk) {
-                const uint4& v = w[j][kk >> 1];
+                const uint4& v = w[sl][j][kk >> 1];
                 bw[j][kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             }
         __builtin_amdgcn_sched_barrier(0);
-        load_w(next);
+        load_w(next, SLOT);
         __builtin_amdgcn_sched_barrier(0);
         constexpr int NF = GPS * MI;
         i32x4 af[2][KPG];
@@ -402,7 +409,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     };
 
     // End of a group for the persistent modes.
-    auto finish_group = [&](int buf, int g) {
+    auto finish_group = [&](int buf, int g) __attribute__((always_inline)) {
         if constexpr (MODE == kPersist) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
@@ -429,35 +436,45 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         (void)g;
     };
 
-    // ---- main loop over K.  Stage ks lives in LDS buffer ks & 1.  Loads past the
-    // last stage are clamped to it (harmless re-reads), so the rotating body is
-    // branch-free.
-    auto step = [&](int ks, auto BUF) {
+    // ---- main loop over K.  Stage ks lives in LDS buffer ks & 1 and, until
+    // then, in register slot ks % PF; step ks issues the loads of stage ks + PF
+    // into the slot stage ks frees.  Loads past the last stage are clamped to it
+    // (harmless re-reads), so the rotating body is branch-free.
+    auto step = [&](int ks, auto BUF, auto SLOT) __attribute__((always_inline)) {
         constexpr int buf = decltype(BUF)::value;
-        const int ahead = min(ks + 1, nks - 1);
-        load_a(ahead);
+        constexpr int sl = decltype(SLOT)::value;
+        const int ahead = min(ks + PF, nks - 1);
+        load_a(ahead, SLOT);
         if constexpr (FINE) {
-            compute_fine(buf, ahead, ks);
+            compute_fine(buf, ahead, ks, SLOT);
         } else if constexpr (ROTATE) {
-            compute(buf, ahead, std::true_type{});
+            compute(buf, ahead, std::true_type{}, SLOT);
         } else {
-            if ((ks % spg) == 0) compute(buf, ahead, std::true_type{});
-            else compute(buf, ahead, std::false_type{});
+            if ((ks % spg) == 0) compute(buf, ahead, std::true_type{}, SLOT);
+            else compute(buf, ahead, std::false_type{}, SLOT);
             if (MODE != kChannel && (ks + 1) % spg == 0) finish_group(buf, ks / spg);
         }
-        store_a(buf ^ 1);
+        store_a(buf ^ 1, std::integral_constant<int, (sl + 1) % PF>{});
         __syncthreads();
     };
-    load_a(0);
-    load_w(0);
-    store_a(0);
+    static_for<0, PF>([&](auto S) __attribute__((always_inline)) {
+        constexpr int s0 = decltype(S)::value;
+        load_a(min(s0, nks - 1), S);
+        load_w(min(s0, nks - 1), S);
+    });
+    store_a(0, std::integral_constant<int, 0>{});
     __syncthreads();
+    constexpr int U = PF == 1 ? 2 : (PF % 2 == 0 ? PF : 2 * PF);  // steps per unrolled round: lcm(2, PF)
     int ks = 0;
-    for (; ks + 2 <= nks; ks += 2) {
-        step(ks, std::integral_constant<int, 0>{});
-        step(ks + 1, std::integral_constant<int, 1>{});
-    }
-    if (ks < nks) step(ks, std::integral_constant<int, 0>{});
+    for (; ks + U <= nks; ks += U)
+        static_for<0, U>([&](auto S) __attribute__((always_inline)) {
+            constexpr int u = decltype(S)::value;
+            step(ks + u, std::integral_constant<int, u & 1>{}, std::integral_constant<int, u % PF>{});
+        });
+    static_for<0, U - 1>([&](auto S) __attribute__((always_inline)) {
+        constexpr int u = decltype(S)::value;
+        if (ks + u < nks) step(ks + u, std::integral_constant<int, u & 1>{}, std::integral_constant<int, u % PF>{});
+    });
 
     if constexpr (MODE == kDump) return;
 
@@ -510,7 +527,12 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS>), dim3(static_cast<unsigned>(tiles)),
+    // Small tiles (one wave per SIMD) have little compute per stage to hide a
+    // load behind: their loads run 4 stages ahead (measured 4-7 % faster at
+    // M = 64..256, N = 8192 for G in {128, 256}, 24 % for G = K).  With G < 128
+    // the deeper ring costs occupancy and time, so those keep one stage.
+    constexpr int PF = (WAVES_M * WAVES_N * MI * NJ <= 8 && GPS == 1) ? 4 : 1;
+    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF>), dim3(static_cast<unsigned>(tiles)),
                        dim3(64 * WAVES_M * WAVES_N), 0, stream, Aq, sa, Wq, sw, static_cast<int>(M),
                        static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
     return hipGetLastError();
