@@ -110,10 +110,13 @@ __device__ __forceinline__ i32x16 splat16(int v) {
     return r;
 }
 
-// One workgroup computes a BM x BN tile with WAVES_M x WAVES_N waves; each
-// wave owns MI x NJ blocks of 32 x 32 (rows x columns).
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
+// One workgroup computes a BM x BN tile with KSPLIT groups of WAVES_M x
+// WAVES_N waves; each wave owns MI x NJ blocks of 32 x 32 (rows x columns).
+// K-group kg runs the contiguous stages [kg nks/KSPLIT, (kg+1) nks/KSPLIT)
+// with LDS buffers of its own, in step with the others (shared barriers); at
+// the end the groups' partial tiles are added through LDS in a fixed order.
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF, int KSPLIT>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
     int32_t* __restrict__ P) {
@@ -128,7 +131,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     static_assert(BM + BN <= NT, "one staged scale per thread");
     static_assert(!FINE || MODE == kRotate || MODE == kDump, "fine groups rotate or dump");
 
-    __shared__ Stage<BM, NT, GPS> st[2];
+    static_assert(KSPLIT == 1 || MODE != kDump, "group sums are dumped per group, K is not split");
+    __shared__ Stage<BM, NT, GPS> st[2][KSPLIT];
 
     // ---- tile selection (XCD-aware) ----
     // Workgroup b runs on XCD b & 7 (round-robin dispatch), each XCD with its
@@ -156,11 +160,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     const int m0 = mt * BM;
     const int n0 = nt * BN;
 
-    const int tid = threadIdx.x;
+    const int kg = KSPLIT == 1 ? 0 : static_cast<int>(threadIdx.x) / NT;  // K-group
+    const int tid = KSPLIT == 1 ? static_cast<int>(threadIdx.x) : static_cast<int>(threadIdx.x) % NT;
     const int wave = tid >> 6, lane = tid & 63;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, lh = lane >> 5;
-    const int nks = K / KS;
+    const int nks = K / KS / KSPLIT;  // stages of this K-group
+    const int kbase = kg * nks;       // its first stage
     const int spg = FINE ? 1 : G / KS;  // stages per group
     const int ng = K / G;
 
@@ -233,12 +239,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         constexpr int sl = decltype(SLOT)::value;
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
-            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0[i]]) = frag2(ra[sl][i].x, ra[sl][i].y);
-            *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1[i]]) = frag2(ra[sl][i].z, ra[sl][i].w);
+            *reinterpret_cast<i32x4*>(&st[buf][kg].a[a_lds0[i]]) = frag2(ra[sl][i].x, ra[sl][i].y);
+            *reinterpret_cast<i32x4*>(&st[buf][kg].a[a_lds1[i]]) = frag2(ra[sl][i].z, ra[sl][i].w);
         }
         if constexpr (MODE != kDump) {
 #pragma unroll
-            for (int gi = 0; gi < GPS; ++gi) st[buf].scale[gi][tid] = rsc[sl][gi];
+            for (int gi = 0; gi < GPS; ++gi) st[buf][kg].scale[gi][tid] = rsc[sl][gi];
         }
     };
     // w[slot][j][kk / 2] holds the two packed dwords of MFMA kk (x, y for even kk, z, w for odd)
@@ -279,17 +285,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
         const int row = wm * MI * 32 + i * 32 + l32;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
-            af[kk] = *reinterpret_cast<const i32x4*>(&st[buf].a[row * AROW + (2 * kk + lh) * 16]);
+            af[kk] = *reinterpret_cast<const i32x4*>(&st[buf][kg].a[row * AROW + (2 * kk + lh) * 16]);
     };
     // Weight scales of this lane's 16 columns in block j (binary16 pairs).
     auto read_sw = [&](int buf, int j, uint2 (&swh)[4], int gi = 0) {
         const int c = BM + wn * NJ * 32 + j * 32 + 4 * lh;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[buf].scale[gi][c + 8 * q]);
+        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[buf][kg].scale[gi][c + 8 * q]);
     };
     // Activation scale of this lane's row in block i, with the 1/256 of the widening.
     auto read_sa = [&](int buf, int i, int gi = 0) {
-        return h2f(st[buf].scale[gi][wm * MI * 32 + i * 32 + l32]) * (1.0f / 256.0f);
+        return h2f(st[buf][kg].scale[gi][wm * MI * 32 + i * 32 + l32]) * (1.0f / 256.0f);
     };
     auto sw_at = [](const uint2 (&swh)[4], int r) {
         const uint32_t pair = (r & 2) ? swh[r >> 2].y : swh[r >> 2].x;
@@ -384,7 +390,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
             const int row = wm * MI * 32 + i * 32 + l32;
 #pragma unroll
             for (int q = 0; q < KPG; ++q)
-                dst[q] = *reinterpret_cast<const i32x4*>(&st[buf].a[row * AROW + (2 * (gi * KPG + q) + lh) * 16]);
+                dst[q] = *reinterpret_cast<const i32x4*>(&st[buf][kg].a[row * AROW + (2 * (gi * KPG + q) + lh) * 16]);
         };
         read_f(0, af[0]);
         uint2 swh[NJ][4];
@@ -443,24 +449,25 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     auto step = [&](int ks, auto BUF, auto SLOT) __attribute__((always_inline)) {
         constexpr int buf = decltype(BUF)::value;
         constexpr int sl = decltype(SLOT)::value;
-        const int ahead = min(ks + PF, nks - 1);
+        const int ahead = kbase + min(ks + PF, nks - 1);
         load_a(ahead, SLOT);
         if constexpr (FINE) {
-            compute_fine(buf, ahead, ks, SLOT);
+            compute_fine(buf, ahead, kbase + ks, SLOT);
         } else if constexpr (ROTATE) {
             compute(buf, ahead, std::true_type{}, SLOT);
         } else {
+            // a K-group's stages start on a group boundary (nks is a multiple of spg)
             if ((ks % spg) == 0) compute(buf, ahead, std::true_type{}, SLOT);
             else compute(buf, ahead, std::false_type{}, SLOT);
-            if (MODE != kChannel && (ks + 1) % spg == 0) finish_group(buf, ks / spg);
+            if (MODE != kChannel && (ks + 1) % spg == 0) finish_group(buf, (kbase + ks) / spg);
         }
         store_a(buf ^ 1, std::integral_constant<int, (sl + 1) % PF>{});
         __syncthreads();
     };
     static_for<0, PF>([&](auto S) __attribute__((always_inline)) {
         constexpr int s0 = decltype(S)::value;
-        load_a(min(s0, nks - 1), S);
-        load_w(min(s0, nks - 1), S);
+        load_a(kbase + min(s0, nks - 1), S);
+        load_w(kbase + min(s0, nks - 1), S);
     });
     store_a(0, std::integral_constant<int, 0>{});
     __syncthreads();
@@ -477,6 +484,37 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     });
 
     if constexpr (MODE == kDump) return;
+
+    // ---- K-groups 1 .. KSPLIT-1 hand their partial tiles to group 0, which adds
+    // them in group order (fp32 sums, or the exact int32 sums of kChannel)
+    if constexpr (KSPLIT > 1) {
+        __shared__ int32_t red[KSPLIT - 1][NT / 64][MI * NJ * 16][64];
+        if (kg > 0) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        if constexpr (MODE == kChannel) red[kg - 1][wave][(i * NJ + j) * 16 + r][lane] = psum[i][j][r];
+                        else red[kg - 1][wave][(i * NJ + j) * 16 + r][lane] = __float_as_int(acc[i][j][r]);
+                    }
+        }
+        __syncthreads();
+        if (kg > 0) return;  // after the workgroup's last barrier
+#pragma unroll
+        for (int k2 = 0; k2 < KSPLIT - 1; ++k2)
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int32_t v = red[k2][wave][(i * NJ + j) * 16 + r][lane];
+                        if constexpr (MODE == kChannel) psum[i][j][r] += v;
+                        else acc[i][j][r] += __int_as_float(v);
+                    }
+    }
 
     // ---- epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3.
     // The last step stored a copy of the final stage (and its scales) into the
@@ -521,9 +559,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void w4a4_gemm_kernel(
     }
 }
 
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
-hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT>
+hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                    int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
@@ -532,18 +570,40 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
     // M = 64..256, N = 8192 for G in {128, 256}, 24 % for G = K).  With G < 128
     // the deeper ring costs occupancy and time, so those keep one stage.
     constexpr int PF = (WAVES_M * WAVES_N * MI * NJ <= 8 && GPS == 1) ? 4 : 1;
-    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF>), dim3(static_cast<unsigned>(tiles)),
-                       dim3(64 * WAVES_M * WAVES_N), 0, stream, Aq, sa, Wq, sw, static_cast<int>(M),
-                       static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
+    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT>),
+                       dim3(static_cast<unsigned>(tiles)), dim3(64 * WAVES_M * WAVES_N * KSPLIT), 0, stream, Aq, sa, Wq,
+                       sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
     return hipGetLastError();
+}
+
+// Small tiles (one wave per SIMD) split K over two wave groups when every CU
+// gets at most one tile and the halves start on group boundaries: two waves
+// per SIMD, half the stages each (MI355X, M = 256, N = 8192: 10 % faster at
+// G = 128, 21 % at G = 256, 11 % at G = K, 28-40 % at G = 32).  With more
+// tiles than CUs the 8-wave workgroups fit once per CU where the 4-wave ones
+// fit twice, and the split loses (N = 10240: 9 % slower).
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
+hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+    constexpr bool small = WAVES_M * WAVES_N * MI * NJ <= 8;
+    if constexpr (small && MODE != kDump) {
+        constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
+        const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+        const int64_t stages = K / KS;
+        const int64_t spg = (MODE == kChannel || GPS > 1) ? 1 : G / KS;
+        if (tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0)
+            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    }
+    return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
 }
 
 }  // namespace
 
 // Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  When that
 // tiling would not give every CU a workgroup, 64 x 128 tiles with 4 waves of
-// 64 x 32 (four times as many workgroups, two per CU).  Up to 32 rows (decode)
-// go to the streaming kernel instead, except for the debug dump.
+// 64 x 32 (four times as many workgroups, two per CU), or 8 waves splitting K
+// (see launch).  One row goes to the dot-product kernel and up to 32 rows
+// (decode) to the streaming kernel instead, except for the debug dump.
 template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                         int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
