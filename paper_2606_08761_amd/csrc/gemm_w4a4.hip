@@ -559,6 +559,227 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     }
 }
 
+// G = 128 on 128 x 256 tiles with a ping-pong schedule.
+//
+// Each SIMD runs one wave of group X (waves 0-3) and one of group Y (waves
+// 4-7), which own the same 128 x 32 outputs per wave as the kernel above.  A
+// wave's stage has an MFMA phase (widen its weights, 16 v_mfma into four
+// group-sum blocks) and a dequant phase (the 4 x 16 elements of those blocks,
+// 2 VALU ops each).  The groups run them half a stage apart, separated by
+// workgroup barriers:
+//     slot 2s:    X: MFMA phase of stage s     Y: dequant of stage s-1
+//     slot 2s+1:  X: dequant of stage s        Y: MFMA phase of stage s
+// (the same loop body for both groups, Y one slot behind)
+// so in every slot one wave of each SIMD issues MFMAs while the other issues
+// VALU work, and the SIMD can run both at once.  The group sums, scales and
+// the order in which groups are added are those of the kernel above, so the
+// results are the same bits.
+//   * A (widened) and the stage's scales are double-buffered in LDS; stage s
+//     sits in buffer s & 1.  X's threads stage rows 0-63 of A and scale slots
+//     0-255, Y's threads rows 64-127 and slots 256-511, each in its own
+//     dequant slot: X writes stage s+1 in slot 2s+1, Y in slot 2s.  Neither
+//     buffer is written while it is read (buffer s & 1 is read in slots 2s and
+//     2s+1 and next written in slots 2s+2 and 2s+3).
+//   * A wave reads its stage's scales in its MFMA phase, so its dequant phase
+//     only touches registers.
+//   * A thread's next global loads are issued as soon as their registers are
+//     free: weights of stage s + 1 right after stage s's are widened, its A
+//     chunk of stage s + 2 right after stage s + 1's is stored (two slots of
+//     cover each).
+__global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
+    const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
+    const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y) {
+    constexpr int NT = 512, BM = 128, BN = 256, MI = 4;
+    __shared__ Stage<BM, NT, 1> st[2];
+
+    // tile selection: as the kernel above
+    const int mt_count = (M + BM - 1) / BM;
+    const int nt_count = (N + BN - 1) / BN;
+    const int T = mt_count * nt_count;
+    int mt, nt;
+    if ((mt_count & 7) == 0 && (nt_count & 7) == 0) {
+        const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+        const int npx = nt_count >> 3;
+        const int band = j / (8 * npx), r = j % (8 * npx);
+        mt = band * 8 + (r & 7);
+        nt = x * npx + (r >> 3);
+    } else {
+        int tile = blockIdx.x;
+        if ((T & 7) == 0) tile = (blockIdx.x & 7) * (T >> 3) + (blockIdx.x >> 3);
+        mt = tile % mt_count;
+        nt = tile / mt_count;
+    }
+    const int m0 = mt * BM, n0 = nt * BN;
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const bool grp_y = wave >= 4;  // uniform per wave
+    const int l32 = lane & 31, lh = lane >> 5;
+    const int nks = K / KS;
+    const int ng = K / 128;
+
+    // this thread's 16-byte chunk of A per stage and its widened LDS places
+    const int ar = tid >> 2, ap = tid & 3;
+    const uint32_t a_off = static_cast<uint32_t>(min(m0 + ar, M - 1)) * static_cast<uint32_t>(K / 2) + ap * 16;
+    const int c0 = 2 * (2 * (ap & 1)) + (ap >> 1);
+    const int a_lds0 = ar * AROW + c0 * 16, a_lds1 = ar * AROW + (c0 + 2) * 16;
+    // this thread's scale slot: an activation row, a weight column or a dummy
+    const bool is_a = tid < BM;
+    const int srow = is_a ? min(m0 + tid, M - 1) : min(n0 + min(tid - BM, BN - 1), N - 1);
+    const uint16_t* sc_base = is_a ? sa : sw;
+    const uint32_t sc_off = static_cast<uint32_t>(srow) * static_cast<uint32_t>(ng);
+    const uint32_t w_off = static_cast<uint32_t>(min(n0 + wave * 32 + l32, N - 1)) * static_cast<uint32_t>(K / 2) + 32 * lh;
+
+    uint4 ra;
+    uint16_t rsc;
+    uint4 w[2];
+    auto load_a = [&](int ks) __attribute__((always_inline)) {
+        ks = min(ks, nks - 1);
+        ra = *reinterpret_cast<const uint4*>(Aq + static_cast<int64_t>(ks) * (KS / 2) + a_off);
+        rsc = sc_base[sc_off + static_cast<uint32_t>(ks)];
+    };
+    auto store_a = [&](int buf) __attribute__((always_inline)) {
+        *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0]) = frag2(ra.x, ra.y);
+        *reinterpret_cast<i32x4*>(&st[buf].a[a_lds1]) = frag2(ra.z, ra.w);
+        st[buf].scale[0][tid] = rsc;
+    };
+    auto load_w = [&](int ks) __attribute__((always_inline)) {
+        ks = min(ks, nks - 1);
+        const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2) + w_off;
+        w[0] = *reinterpret_cast<const uint4*>(base);
+        w[1] = *reinterpret_cast<const uint4*>(base + 16);
+    };
+
+    f32x16 acc[MI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+    i32x16 D[MI];
+    uint2 swh[4];
+    float sav[MI];
+    const i32x16 start = splat16(static_cast<int>(MAGIC_BITS));
+
+    // MFMA phase of stage s (LDS buffer and register slot s & 1)
+    auto mfma_phase = [&](int s, int par) __attribute__((always_inline)) {
+        const int c = BM + wave * 32 + 4 * lh;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[par].scale[0][c + 8 * q]);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) sav[i] = h2f(st[par].scale[0][i * 32 + l32]) * (1.0f / 256.0f);
+        i32x4 bw[KK];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            const uint4& v = w[kk >> 1];
+            bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(s + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        // the four blocks' chains interleaved, MFMA n = (kk = n / 4, i = n % 4)
+        // needs (i, kk - 1) only, four MFMAs earlier; A fragments are read LA
+        // MFMAs ahead into a ring of LA + 1
+        constexpr int LA = 4;
+        i32x4 af[LA + 1];
+        auto frag = [&](int n) __attribute__((always_inline)) {
+            const int kk = n >> 2, i = n & 3;
+            return *reinterpret_cast<const i32x4*>(&st[par].a[(i * 32 + l32) * AROW + (2 * kk + lh) * 16]);
+        };
+        static_for<0, LA>([&](auto NN) __attribute__((always_inline)) { af[decltype(NN)::value] = frag(decltype(NN)::value); });
+        static_for<0, 4 * MI>([&](auto NN) __attribute__((always_inline)) {
+            constexpr int n = decltype(NN)::value;
+            if constexpr (n + LA < 4 * MI) af[(n + LA) % (LA + 1)] = frag(n + LA);
+            constexpr int kk = n >> 2, i = n & 3;
+            D[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[kk], af[n % (LA + 1)], kk == 0 ? start : D[i], 0, 0, 0);
+        });
+        // keep that order: LA fragment reads, then MFMA / next read pairs
+        __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
+        static_for<0, 4 * MI - LA>([&](auto) __attribute__((always_inline)) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        });
+        __builtin_amdgcn_sched_group_barrier(0x008, LA, 0);
+    };
+    // acc += fl(P s_a) * s_w for the four blocks of the last MFMA phase
+    auto dequant_phase = [&]() __attribute__((always_inline)) {
+        // opaque to the optimizer: no part of the dequantization moves above
+        // the barrier into the MFMA phase (where it would wait for the MFMAs)
+#pragma unroll
+        for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(D[i]));
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const float nb = -MAGIC * sav[i];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const uint32_t pair = (r & 2) ? swh[r >> 2].y : swh[r >> 2].x;
+                const uint16_t hw = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
+                const float t = fmaf(__int_as_float(D[i][r]), sav[i], nb);
+                acc[i][r] = fmaf(t, h2f(hw), acc[i][r]);
+            }
+        }
+    };
+    // this thread's part of stage t (in its registers) into LDS, then the
+    // loads of stage t + 1
+    auto stage_next = [&](int t) __attribute__((always_inline)) {
+        store_a(t & 1);
+        load_a(t + 1);
+    };
+
+    // prologue: stage 0 in LDS buffer 0 (every thread), stage 1 in registers
+    load_w(0);
+    load_a(0);
+    store_a(0);
+    load_a(1);
+    __syncthreads();
+
+    // Both groups run the same loop body, Y one slot behind X: Y spends slot 0
+    // staging its half of stage 1, and X ends with one barrier more, so the
+    // barrier counts match.  In its dequant slot of stage s, X stages its half
+    // of stage s + 1 and Y its half of stage s + 2.  The compiler keeps each
+    // phase between its barriers (no code motion across them).
+    if (grp_y) {
+        stage_next(1);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+    }
+    const int ahead = grp_y ? 2 : 1;
+    for (int s = 0; s < nks; ++s) {
+        mfma_phase(s, s & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        dequant_phase();
+        stage_next(s + ahead);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+    }
+    if (!grp_y) __syncthreads();
+
+    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+        const int gm = m0 + i * 32 + l32;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t h01 = __half_as_ushort(__float2half_rn(acc[i][4 * q + 0])) |
+                                 (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(acc[i][4 * q + 1]))) << 16);
+            const uint32_t h23 = __half_as_ushort(__float2half_rn(acc[i][4 * q + 2])) |
+                                 (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(acc[i][4 * q + 3]))) << 16);
+            const int gn = n0 + wave * 32 + 8 * q + 4 * lh;
+            if (gm < M) {
+                uint16_t* dst = Y + static_cast<int64_t>(gm) * N + gn;
+                if ((N & 3) == 0 && gn + 3 < N) {
+                    *reinterpret_cast<uint2*>(dst) = make_uint2(h01, h23);
+                } else {
+                    if (gn + 0 < N) dst[0] = static_cast<uint16_t>(h01 & 0xFFFFu);
+                    if (gn + 1 < N) dst[1] = static_cast<uint16_t>(h01 >> 16);
+                    if (gn + 2 < N) dst[2] = static_cast<uint16_t>(h23 & 0xFFFFu);
+                    if (gn + 3 < N) dst[3] = static_cast<uint16_t>(h23 >> 16);
+                }
+            }
+        }
+    }
+}
+
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT>
 hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                     int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
@@ -616,7 +837,16 @@ hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq
     if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    if (G == 128) return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 128) {
+        if constexpr (WAVES_N == 8 && MI == 4) {
+            const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+            if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+            hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, Aq, sa, Wq,
+                               sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+            return hipGetLastError();
+        }
+        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    }
     if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
 }
