@@ -702,8 +702,6 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     };
     // acc += fl(P s_a) * s_w for the four blocks of the last MFMA phase
     auto dequant_phase = [&]() __attribute__((always_inline)) {
-        // opaque to the optimizer: no part of the dequantization moves above
-        // the barrier into the MFMA phase (where it would wait for the MFMAs)
 #pragma unroll
         for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(D[i]));
 #pragma unroll
@@ -743,11 +741,19 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
         __syncthreads();
     }
     const int ahead = grp_y ? 2 : 1;
+    // The empty asm statements make the MFMA results and the accumulators
+    // opaque at the barriers, so that no MFMA or dequant work is sunk past the
+    // barrier that ends its phase (or hoisted above the one that starts it).
+    auto pin = [](auto& v) __attribute__((always_inline)) { asm volatile("" : "+v"(v)); };
     for (int s = 0; s < nks; ++s) {
         mfma_phase(s, s & 1);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) pin(D[i]);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         dequant_phase();
+#pragma unroll
+        for (int i = 0; i < MI; ++i) pin(acc[i]);
         stage_next(s + ahead);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
