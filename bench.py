@@ -69,6 +69,11 @@ def parse():
     return p.parse_args()
 
 
+def is_tiled_gemm(name: str) -> bool:
+    """Kernel-trace / counter rows of the tiled GEMM (both G = 128 ping-pong and the general kernel)."""
+    return "w4a4_gemm_kernel" in name or "w4a4_gemm_pp_kernel" in name
+
+
 def traffic_from_profile():
     """HBM bytes per GEMM launch from the committed counter summary, if it was
     taken on the current kernel source; else None."""
@@ -151,7 +156,7 @@ def summarize_mode(args):
     fetch = per_kernel(args.fetch_csv, "FETCH_SIZE")
     write = per_kernel(args.write_csv, "WRITE_SIZE")
     f_copy, w_copy = pick(fetch, "copy_kernel"), pick(write, "copy_kernel")
-    f_gemm, w_gemm = pick(fetch, "w4a4_gemm_kernel"), pick(write, "w4a4_gemm_kernel")
+    f_gemm, w_gemm = pick(fetch, "w4a4_gemm_pp_kernel"), pick(write, "w4a4_gemm_pp_kernel")
     f_scale, w_scale = copy_kib / f_copy, copy_kib / w_copy
     read_b = f_gemm * f_scale * 1024.0
     write_b = w_gemm * w_scale * 1024.0
@@ -160,7 +165,7 @@ def summarize_mode(args):
     stats = list(csv.DictReader(open(args.stats_csv)))
     cmds = open(args.commands).read().strip() if args.commands else ""
     prof = {
-        "kernel": "w4a4_gemm_kernel (G=128 rotating mode)",
+        "kernel": "w4a4_gemm_pp_kernel (G=128, 128 x 256 tiles, ping-pong)",
         "workload": f"M={M} N={N} K={K} G={G}",
         "kernel_source_sha256": hashlib.sha256(open(src, "rb").read()).hexdigest(),
         "fetch_kib_per_dispatch": f_gemm, "write_kib_per_dispatch": w_gemm,
@@ -369,7 +374,7 @@ def summarize_sq(paths, cmds):
     vals = {}
     for p in paths:
         for r in csv.DictReader(open(p)):
-            if "w4a4_gemm_kernel" not in r["Kernel_Name"]:
+            if not is_tiled_gemm(r["Kernel_Name"]):
                 continue
             vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     c = {k: statistics.mean(v) for k, v in vals.items()}
@@ -531,14 +536,14 @@ def summarize_gsweep(trace_csv, pmc_csv, cmds):
         assert len(ids) == GSWEEP_LAUNCHES * len(Gs), (len(ids), "GEMM dispatches")
         return {d: Gs[i // GSWEEP_LAUNCHES] for i, d in enumerate(ids)}
 
-    trace = [r for r in csv.DictReader(open(trace_csv)) if "w4a4_gemm_kernel" in r["Kernel_Name"]]
+    trace = [r for r in csv.DictReader(open(trace_csv)) if is_tiled_gemm(r["Kernel_Name"])]
     gmap = by_position({int(r["Dispatch_Id"]) for r in trace})
     durs = {}
     for r in trace:
         durs.setdefault(gmap[int(r["Dispatch_Id"])], []).append(
             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     times = {g: statistics.median(v) for g, v in durs.items()}
-    rows = [r for r in csv.DictReader(open(pmc_csv)) if "w4a4_gemm_kernel" in r["Kernel_Name"]]
+    rows = [r for r in csv.DictReader(open(pmc_csv)) if is_tiled_gemm(r["Kernel_Name"])]
     pmap = by_position({int(r["Dispatch_Id"]) for r in rows})
     cnt = {}
     for r in rows:
@@ -865,7 +870,7 @@ def main():
                    "rotating_input_sets": R},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS,
                      "unit": "TOP/s", "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": traffic_from_profile(), "kernel": "w4a4_gemm_kernel",
+                     "traffic": traffic_from_profile(), "kernel": "w4a4_gemm_pp_kernel",
                      "kernel_us": round(gemm_ms * 1e3, 3)},
         "quant_us": round(quant_ms * 1e3, 3),
         "quant_hbm_gbs": round((2.5 * M * K + 2 * M * K / G) / (quant_ms * 1e-3) / 1e9, 1),
