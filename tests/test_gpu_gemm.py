@@ -42,6 +42,20 @@ def test_tiny_workload_full(O):
     check_tolerance(run_gemm(Aq, sa, Wq, sw, G), O.gemm_rows(Aq, sa, Wq, sw, K, G), "tiny")
 
 
+# Ragged shapes with at least one 128 x 256 tile per CU: G = 128 runs the
+# ping-pong kernel there (partial M and N tiles, odd N, an odd stage count).
+BIG_RAGGED = [(1111, 8200, 640, 128), (1500, 8195, 1152, 128), (2050, 4100, 4096, 128)]
+
+
+@pytest.mark.parametrize("M,N,K,G", BIG_RAGGED)
+def test_big_ragged_shapes(O, M, N, K, G):
+    log(f"big ragged M={M} N={N} K={K} G={G}")
+    r = np.random.default_rng(M * 7919 + N * 31 + K + G + 1)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+    check_tolerance(run_gemm(Aq, sa, Wq, sw, G), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"big ragged {M}x{N}x{K} G{G}")
+
+
 RAGGED = [
     (1, 128, 128, 128), (8, 200, 256, 128), (33, 1024, 1024, 256), (129, 136, 512, 512),
     (2, 64, 1024, 1024), (300, 260, 384, 128), (64, 1024, 1024, 1024), (17, 8, 256, 256),
