@@ -47,6 +47,11 @@
 //   * Workgroup ids are remapped so that each XCD (8 per MI355X, each with its
 //     own L2) works on a compact block of output tiles (8 m-tiles by a band of
 //     n-tiles at a time).
+//   * G == 128 on 128 x 256 tiles runs w4a4_gemm_pp_kernel: the same wave tile
+//     and arithmetic, with the two waves of each SIMD running their MFMA and
+//     dequant phases half a stage apart (described at the kernel).  Small tiles
+//     (64 x 128) may split K over two wave groups (KSPLIT) and keep PF stages
+//     of loads in flight.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
