@@ -9,7 +9,7 @@
 //     round-robin (wave w takes stages w, w + 8, ...), so neighbouring waves read
 //     neighbouring 64-byte runs of every weight row.
 //   * Each wave streams (tile, stage) pairs through a ring of PF stages of packed
-//     weights, activations and weight scales held in registers.  The ring runs
+//     weights and activations held in registers.  The ring runs
 //     across tile boundaries, so the next tile's loads are in flight while a tile
 //     is reduced and stored.  Every wave walks the same number of stages per
 //     tile: stages past K are re-reads of the last one with weight 0, which
