@@ -28,7 +28,9 @@
  * (M-sized when M == 0, the group-sum dump when mr == 0) may be NULL.  A failed launch returns
  * APEX4_ERR_LAUNCH.  Nothing is written when validation fails.
  *
- * Shape rules:  M >= 0, N >= 1, K >= 128 and K % 128 == 0, K % G == 0.
+ * Shape rules:  M >= 0, N >= 1, K >= 128 and K % 128 == 0, K % G == 0; each
+ * packed operand of the GEMM entry points under 4 GiB (M K/2 and N K/2 below
+ * 2^32 bytes).
  * Group sizes: the GEMM takes G in {32, 64, 128, 256, 512, 1024} or G == K
  * (per-channel); these are the granularities of Sec. 3.2.2 and Sec. 4.1.  The
  * quantizer takes any G with G % 32 == 0 and K % G == 0.

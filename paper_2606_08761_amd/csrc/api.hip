@@ -36,6 +36,8 @@ int check_device() {
 int check_gemm_shape(int64_t M, int64_t N, int64_t K) {
     if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
     if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    // the kernels address a packed operand row by row with 32-bit byte offsets
+    if (M * (K / 2) > 0xFFFFFFFFll || N * (K / 2) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
     return APEX4_OK;
 }
 

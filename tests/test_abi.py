@@ -108,6 +108,8 @@ def test_gemm_validation(L):
     assert g(*ok, 4, 8, 4096, 2048, h.ptr(), s) == -3
     assert g(*ok, 4, 8, 1024, 1000, h.ptr(), s) == -3
     assert g(*ok, 4, 8, 384, 256, h.ptr(), s) == -2                # K % G
+    assert g(*ok, 1 << 20, 8, 1 << 13, 128, h.ptr(), s) == -2      # A_q of 4 GiB
+    assert g(*ok, 4, 1 << 21, 1 << 12, 128, h.ptr(), s) == -2      # W_q of 4 GiB
     assert g(h.ptr(1), *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -4
     assert g(*ok, 4, 8, 256, 128, h.ptr(2), s) == -4
 
