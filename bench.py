@@ -829,7 +829,30 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     codes_gemm_ms = e0.elapsed_time(e1) / reps
-    del c, Yc
+
+    # ---- the same GEMM on the FP6 matrix cores (codes re-encoded as e3m2) ----
+    A6, W6 = pk.apex4_pack_fp6(c[0]), pk.apex4_pack_fp6(c[2])
+    Y6 = torch.empty_like(Yc)
+    for _ in range(5):
+        pk.apex4_w4a4_gemm_fp6(A6, c[1], W6, c[3], G, Y6)
+    e0.record(stream)
+    for _ in range(reps):
+        pk.apex4_w4a4_gemm_fp6(A6, c[1], W6, c[3], G, Y6)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fp6_ms = e0.elapsed_time(e1) / reps
+    e0.record(stream)
+    for _ in range(reps):
+        pk.apex4_pack_fp6(c[0], A6)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    pack_ms = e0.elapsed_time(e1) / reps
+    fp6 = {"gemm_us": round(fp6_ms * 1e3, 3), "tops": round(2.0 * M * N * K / (fp6_ms * 1e-3) / 1e12, 2),
+           "time_vs_int8_kernel": round(fp6_ms / codes_gemm_ms, 3),
+           "same_bits_as_int8_kernel": bool(torch.equal(Y6.view(torch.int16), Yc.view(torch.int16))),
+           "pack_activations_us": round(pack_ms * 1e3, 3),
+           "mfma": "v_mfma_scale_f32_32x32x64_f8f6f4, FP6 e3m2 operands, unit E8M0 scales"}
+    del c, Yc, A6, W6, Y6
 
     # ---- fp16 GEMM of the same shape (torch -> hipBLASLt), rotated too ----
     fsets = []
@@ -883,6 +906,7 @@ def main():
         "fp16_gemm_tflops": round(ops / (fp16_ms * 1e-3) / 1e12, 2),
         "speedup_gemm_vs_fp16": round(fp16_ms / gemm_ms, 3),
         "speedup_step_vs_fp16": round(fp16_ms / ms_per_step, 3),
+        "fp6_variant": fp6,
     }
     if not args.no_decode:
         line["decode"] = decode_bench()

@@ -122,6 +122,36 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
                       int64_t M, int64_t N, int64_t K, int64_t G,
                       void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
 
+/*
+ * Re-encode packed 4-bit codes as FP6 e3m2 codes for apex4_w4a4_gemm_fp6.
+ * Every code q in [-8, 7] is exact in FP6 e3m2 (1 sign, 3 exponent with bias 3,
+ * 2 mantissa bits); this is a change of container for the codes of Sec. 3.2.1,
+ * not of their values, made once per weight matrix (Alg. 1 quantizes weights
+ * offline) and per activation batch.
+ *
+ *   q4 [rows, K/2] packed codes as above (device, read-only);
+ *   q6 [rows, 3K/4] (device, output): code k of a row in bits [6k, 6k + 6) of
+ *   the row's bytes read as a little-endian bit string.
+ * rows >= 0; K >= 128, K % 128 == 0; rows == 0 is a no-op.
+ */
+int apex4_pack_fp6(const uint8_t* q4, int64_t rows, int64_t K, uint8_t* q6, void* stream);
+
+/*
+ * apex4_w4a4_gemm on FP6 containers: the same Y, bit for bit, from the codes
+ * re-encoded by apex4_pack_fp6 (Eq. (group_decomposition); the group sums are
+ * exact on the FP6 matrix cores, whose products and fp32 sums of at most 128
+ * products of codes are integers below 2^24).
+ *
+ *   A_6 [M, 3K/4], W_6 [N, 3K/4] FP6 codes; s_a [M, K/G], s_w [N, K/G] binary16
+ *   scales (device, read-only); Y [M, N] binary16 (device, output).
+ * G == 128 only (APEX4_ERR_GROUP otherwise); each FP6 operand under 4 GiB
+ * (M 3K/4 and N 3K/4 below 2^32 bytes); other rules as apex4_w4a4_gemm.
+ */
+int apex4_w4a4_gemm_fp6(const uint8_t* A_6, const void* s_a,
+                        const uint8_t* W_6, const void* s_w,
+                        int64_t M, int64_t N, int64_t K, int64_t G,
+                        void* Y, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* apex4_status_string(int status);
 

@@ -25,7 +25,8 @@ STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4
           -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-            "apex4_w4a4_linear", "apex4_status_string", "apex4_version")
+            "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_status_string",
+            "apex4_version")
 
 _lib = None
 
@@ -50,7 +51,10 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm.argtypes = [P, P, P, P, I, I, I, I, P, P]
     L.apex4_w4a4_gemm_groupsums.argtypes = [P, P, I, I, I, I, I, I, P, P]
     L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
-    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear"):
+    L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
+    L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
+    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear",
+              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -145,6 +149,32 @@ def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None,
                                  _dev(Y, torch.float16, "Y"), _dev(A_q_work, torch.uint8, "A_q_work"),
                                  _dev(s_a_work, torch.float16, "s_a_work"), _stream(x, stream))
     _check("apex4_w4a4_linear", rc)
+    return Y
+
+
+def apex4_pack_fp6(q4, q6=None, stream=None):
+    """Packed 4-bit codes uint8 [rows, K/2] -> FP6 e3m2 codes uint8 [rows, 3K/4]."""
+    import torch
+    rows, K2 = q4.shape
+    K = 2 * K2
+    if q6 is None:
+        q6 = torch.empty((rows, 3 * K // 4), dtype=torch.uint8, device=q4.device)
+    rc = lib().apex4_pack_fp6(_dev(q4, torch.uint8, "q4"), rows, K, _dev(q6, torch.uint8, "q6"), _stream(q4, stream))
+    _check("apex4_pack_fp6", rc)
+    return q6
+
+
+def apex4_w4a4_gemm_fp6(A_6, s_a, W_6, s_w, G: int, Y=None, stream=None):
+    """apex4_w4a4_gemm on FP6 containers (A_6 [M, 3K/4], W_6 [N, 3K/4]); G = 128."""
+    import torch
+    M, K34 = A_6.shape
+    N = W_6.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_6.device)
+    rc = lib().apex4_w4a4_gemm_fp6(_dev(A_6, torch.uint8, "A_6"), _dev(s_a, torch.float16, "s_a"),
+                                   _dev(W_6, torch.uint8, "W_6"), _dev(s_w, torch.float16, "s_w"),
+                                   M, N, 4 * K34 // 3, G, _dev(Y, torch.float16, "Y"), _stream(A_6, stream))
+    _check("apex4_w4a4_gemm_fp6", rc)
     return Y
 
 

@@ -42,4 +42,10 @@ bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N,
                                int64_t K, int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream);
 
+// The 4-bit codes in FP6 e3m2 containers (6-bit fields, little-endian, 3K/4
+// bytes per row) and the G = 128 GEMM on the FP6 matrix cores that reads them.
+hipError_t launch_pack_fp6(const uint8_t* q4, int64_t rows, int64_t K, uint8_t* q6, hipStream_t stream);
+hipError_t launch_gemm_fp6(const uint8_t* A6, const uint16_t* sa, const uint8_t* W6, const uint16_t* sw, int64_t M,
+                           int64_t N, int64_t K, uint16_t* Y, hipStream_t stream);
+
 }  // namespace apex4

@@ -162,4 +162,34 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 
+int apex4_pack_fp6(const uint8_t* q4, int64_t rows, int64_t K, uint8_t* q6, void* stream) {
+    if (!present(q4, rows) || !present(q6, rows)) return APEX4_ERR_NULL;
+    if (rows < 0 || K < 128 || (K % 128) != 0 || rows > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (!aligned16(q4) || !aligned16(q6)) return APEX4_ERR_ALIGN;
+    const int rc = check_device();
+    if (rc) return rc;
+    if (rows == 0) return APEX4_OK;
+    const hipError_t e = apex4::launch_pack_fp6(q4, rows, K, q6, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_fp6(const uint8_t* A_6, const void* s_a, const uint8_t* W_6, const void* s_w, int64_t M,
+                        int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+    if (!present(A_6, M) || !present(s_a, M) || !W_6 || !s_w || !present(Y, M)) return APEX4_ERR_NULL;
+    if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    // 32-bit byte offsets into each FP6 operand
+    if (M * (3 * K / 4) > 0xFFFFFFFFll || N * (3 * K / 4) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
+    if (G != 128) return APEX4_ERR_GROUP;
+    if (!aligned16(A_6) || !aligned16(s_a) || !aligned16(W_6) || !aligned16(s_w) || !aligned16(Y))
+        return APEX4_ERR_ALIGN;
+    const int rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const hipError_t e = apex4::launch_gemm_fp6(A_6, static_cast<const uint16_t*>(s_a), W_6,
+                                                static_cast<const uint16_t*>(s_w), M, N, K,
+                                                static_cast<uint16_t*>(Y), static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
 }  // extern "C"

@@ -36,7 +36,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-              "apex4_w4a4_linear", "apex4_status_string", "apex4_version"):
+              "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_status_string",
+              "apex4_version"):
         assert f in names
 
 
@@ -136,6 +137,28 @@ def test_linear_validation(L):
     assert f(*args(), 4, 8, 200, 128, h.ptr(), h.ptr(), h.ptr(), s) == -2
     assert f(*args(), 4, 8, 384, 96, h.ptr(), h.ptr(), h.ptr(), s) == -3
     assert f(*args(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -4
+
+
+def test_fp6_validation(L):
+    h = Host()
+    f = L.apex4_pack_fp6
+    s = NULL
+    assert f(NULL, 4, 256, h.ptr(), s) == -1
+    assert f(h.ptr(), 4, 256, NULL, s) == -1
+    assert f(h.ptr(), -1, 256, h.ptr(), s) == -2
+    assert f(h.ptr(), 4, 200, h.ptr(), s) == -2                     # K % 128
+    assert f(h.ptr(8), 4, 256, h.ptr(), s) == -4
+    g = L.apex4_w4a4_gemm_fp6
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -1
+    assert g(*ok, 4, 8, 256, 128, NULL, s) == -1
+    assert g(*ok, 4, 0, 256, 128, h.ptr(), s) == -2
+    assert g(*ok, 4, 8, 320, 128, h.ptr(), s) == -2                # K % 128
+    assert g(*ok, 4, 8, 256, 64, h.ptr(), s) == -3                 # G = 128 only
+    assert g(*ok, 4, 8, 256, 256, h.ptr(), s) == -3
+    assert g(*ok, 1 << 20, 8, 6144, 128, h.ptr(), s) == -2         # A_6 of 4.5 GiB
+    assert g(*ok, 4, 1 << 21, 4096, 128, h.ptr(), s) == -2         # W_6 of 6 GiB
+    assert g(h.ptr(4), *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -4
 
 
 def test_device_check_without_gpu():
