@@ -249,7 +249,9 @@ def layers_mode(reps: int = 10):
     (torch.matmul -> hipBLASLt).  Weights are rotated over at least 512 MB of
     copies (twice the Infinity Cache); codes and scales are random (speed does
     not depend on values).  The W4A4 linears are timed from a replayed graph of
-    `reps` calls (GPU time, no Python launch overhead), the fp16 GEMMs eagerly."""
+    `reps` calls (GPU time, no Python launch overhead), the fp16 GEMMs eagerly.
+    Where the G=128 GEMM is split over K the linear is the quantizer followed by
+    apex4_w4a4_gemm_ws with a workspace, as W4A4Linear runs it."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import workloads as wl
@@ -300,7 +302,7 @@ def layers_mode(reps: int = 10):
             R = copies(Nl * Kl // 2 + 2 * Nl * (Kl // Gv))
             wsets[name] = [(Wq, sw)] + [(Wq.clone(), sw.clone()) for _ in range(R - 1)]
         for Ml in LAYER_M:
-            per, gbs = {}, {}
+            per, gbs, split = {}, {}, {}
             for name, Nl, Kl, Gl in linears:
                 Gv = Gl or Kl
                 x = torch.from_numpy(wl.activations(wl.rng_for("llama70b", 98, Ml + Kl), Ml, Kl)).to(dev)
@@ -308,15 +310,26 @@ def layers_mode(reps: int = 10):
                 Aq = torch.empty((Ml, Kl // 2), dtype=torch.uint8, device=dev)
                 sa = torch.empty((Ml, Kl // Gv), dtype=torch.float16, device=dev)
                 ws = wsets[name]
-                t = graph_timed(lambda i: pk.apex4_w4a4_linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa),
-                                reps)
+                need = pk.apex4_w4a4_gemm_workspace_size(Ml, Nl, Kl, Gv)
+                if need:
+                    # as W4A4Linear: quantize, then the GEMM split over K with a workspace
+                    work = torch.empty((need,), dtype=torch.uint8, device=dev)
+
+                    def call(i):
+                        pk.apex4_quantize_act(x, Gv, Aq, sa)
+                        pk.apex4_w4a4_gemm_ws(Aq, sa, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, work, Y)
+                else:
+                    def call(i):
+                        pk.apex4_w4a4_linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa)
+                t = graph_timed(call, reps)
+                split[name] = need // (4 * Ml * Nl) if need else 1
                 per[name] = round(t, 2)
                 # algorithmic HBM bytes of the linear: x, codes, scales, Y
                 nbytes = 2 * Ml * Kl + Ml * Kl / 2 + Nl * Kl / 2 + 2 * (Ml + Nl) * Kl / Gv + 2 * Ml * Nl
                 gbs[name] = round(nbytes / (t * 1e-6) / 1e9)
                 del x, Y, Aq, sa
             print(json.dumps({"mode": "layers", "config": cfg, "M": Ml, "linear_us": per, "hbm_gbs": gbs,
-                              "total_us": round(sum(per.values()), 2)}), flush=True)
+                              "k_splits": split, "total_us": round(sum(per.values()), 2)}), flush=True)
         del wsets
         torch.cuda.empty_cache()
     # fp16 GEMMs of the same shapes (the value projection is part of qkv)
@@ -340,8 +353,9 @@ def summarize_layers(path, command):
     tot = {(r["config"], r["M"]): r for r in rows}
     lines = ["# Llama-2-70B decoder-layer linears: uniform G=128 vs mixed granularity vs fp16", "",
              "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
-             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear) "
-             "from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
+             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear, or "
+             "apex4_quantize_act + apex4_w4a4_gemm_ws where the G=128 GEMM is split over K into S "
+             "ranges, marked S=) from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
              "torch.matmul (hipBLASLt) on the same shapes, rotated the same way, timed eagerly. "
              "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
              "share one per-channel GEMM (N=9216).", "",
@@ -356,9 +370,10 @@ def summarize_layers(path, command):
     lines += ["", "Per linear (us; W4A4 rows also give the algorithmic HBM GB/s of x, codes, scales and Y):", "",
               "| config | M | per linear |", "|---|---|---|"]
     for r in rows:
-        g = r.get("hbm_gbs", {})
+        g, sp = r.get("hbm_gbs", {}), r.get("k_splits", {})
         lines.append(f"| {r['config']} | {r['M']} | " +
-                     ", ".join(f"{k} {v}" + (f" ({g[k]} GB/s)" if k in g else "") for k, v in r["linear_us"].items()) + " |")
+                     ", ".join(f"{k} {v}" + (f" ({g[k]} GB/s)" if k in g else "") +
+                               (f" S={sp[k]}" if sp.get(k, 1) > 1 else "") for k, v in r["linear_us"].items()) + " |")
     with open(os.path.join(ROOT, "profiles", "layer_sweep_llama2_70b.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 

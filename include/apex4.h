@@ -53,7 +53,8 @@ typedef enum {
     APEX4_ERR_GROUP = -3,   /* unsupported group size G */
     APEX4_ERR_ALIGN = -4,   /* a pointer is not 16-byte aligned */
     APEX4_ERR_LAUNCH = -5,  /* the HIP launch failed */
-    APEX4_ERR_DEVICE = -6   /* no device, or the current device is not gfx950 */
+    APEX4_ERR_DEVICE = -6,  /* no device, or the current device is not gfx950 */
+    APEX4_ERR_WORKSPACE = -7 /* workspace NULL or smaller than the size query returns */
 } apex4_status;
 
 /*
@@ -121,6 +122,33 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
 int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
                       int64_t M, int64_t N, int64_t K, int64_t G,
                       void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
+
+/*
+ * Workspace form of apex4_w4a4_gemm for shapes that leave compute units idle
+ * (Eq. (group_decomposition) split over K; the striped work decomposition of
+ * Sec. 4.2 across workgroups).  When the 128 x 256 tiles of a G = 128 GEMM
+ * number fewer than the compute units (M > 32), K is split into S in {2, 4, 8}
+ * ranges of whole groups; each workgroup writes an fp32 partial tile into the
+ * workspace, and a second kernel sums the S partials in range order and rounds
+ * once to binary16.  Y is then within the tolerance of apex4_w4a4_gemm (the
+ * fp32 summation order differs), deterministic for a given shape and device.
+ *
+ * apex4_w4a4_gemm_workspace_size writes to *bytes the workspace this shape
+ * needs on the current device: S * M * N * 4, or 0 where no split applies (then
+ * apex4_w4a4_gemm_ws is apex4_w4a4_gemm and workspace may be NULL).
+ *
+ *   workspace: caller-owned device memory, 16-byte aligned, at least *bytes
+ *   long; overwritten; must not alias the operands.  Calls that share a
+ *   workspace must be ordered on one stream.
+ * Errors as apex4_w4a4_gemm, plus APEX4_ERR_WORKSPACE when the workspace is
+ * needed and NULL or shorter than the size query returns (checked last, after
+ * the device, since the split depends on the device's compute-unit count).
+ */
+int apex4_w4a4_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int64_t G, int64_t* bytes);
+int apex4_w4a4_gemm_ws(const uint8_t* A_q, const void* s_a,
+                       const uint8_t* W_q, const void* s_w,
+                       int64_t M, int64_t N, int64_t K, int64_t G,
+                       void* Y, void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
  * Re-encode packed 4-bit codes as FP6 e3m2 codes for apex4_w4a4_gemm_fp6.

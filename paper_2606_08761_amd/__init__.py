@@ -25,8 +25,8 @@ STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4
           -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-            "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_status_string",
-            "apex4_version")
+            "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
+            "apex4_w4a4_gemm_ws", "apex4_status_string", "apex4_version")
 
 _lib = None
 
@@ -52,9 +52,11 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm_groupsums.argtypes = [P, P, I, I, I, I, I, I, P, P]
     L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
     L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
+    L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
+    L.apex4_w4a4_gemm_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear",
-              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6"):
+              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -114,6 +116,33 @@ def apex4_w4a4_gemm(A_q, s_a, W_q, s_w, G: int, Y=None, stream=None):
                                _dev(W_q, torch.uint8, "W_q"), _dev(s_w, torch.float16, "s_w"),
                                M, N, 2 * K2, G, _dev(Y, torch.float16, "Y"), _stream(A_q, stream))
     _check("apex4_w4a4_gemm", rc)
+    return Y
+
+
+def apex4_w4a4_gemm_workspace_size(M: int, N: int, K: int, G: int) -> int:
+    """Bytes of workspace apex4_w4a4_gemm_ws needs for this shape on the current device (0: none)."""
+    b = ctypes.c_int64(0)
+    _check("apex4_w4a4_gemm_workspace_size", lib().apex4_w4a4_gemm_workspace_size(M, N, K, G, ctypes.byref(b)))
+    return int(b.value)
+
+
+def apex4_w4a4_gemm_ws(A_q, s_a, W_q, s_w, G: int, workspace=None, Y=None, stream=None):
+    """apex4_w4a4_gemm split over K when its tiles leave CUs idle; workspace is a
+    uint8 device tensor of at least apex4_w4a4_gemm_workspace_size bytes (made
+    here when None)."""
+    import torch
+    M, K2 = A_q.shape
+    N, K = W_q.shape[0], 2 * K2
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
+    if workspace is None:
+        need = apex4_w4a4_gemm_workspace_size(M, N, K, G)
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=A_q.device)
+    rc = lib().apex4_w4a4_gemm_ws(_dev(A_q, torch.uint8, "A_q"), _dev(s_a, torch.float16, "s_a"),
+                                  _dev(W_q, torch.uint8, "W_q"), _dev(s_w, torch.float16, "s_w"),
+                                  M, N, K, G, _dev(Y, torch.float16, "Y"), _dev(workspace, torch.uint8, "workspace"),
+                                  workspace.numel(), _stream(A_q, stream))
+    _check("apex4_w4a4_gemm_ws", rc)
     return Y
 
 
@@ -191,9 +220,10 @@ class W4A4Linear:
         lin = W4A4Linear(weight_fp16_cuda, G=128)
         y = lin(x)             # x [..., K] float16 on the same device -> [..., N]
 
-    The work buffers for the quantized activations are kept and reused while
-    the row count stays the same.  Bias and other dtypes are not supported:
-    the paper's layers are bias-free fp16 linears."""
+    The work buffers for the quantized activations (and, for row counts whose
+    G = 128 GEMM is split over K, its workspace) are kept and reused while the
+    row count stays the same.  Bias and other dtypes are not supported: the
+    paper's layers are bias-free fp16 linears."""
 
     def __init__(self, weight, G: int = 128):
         import torch
@@ -214,7 +244,14 @@ class W4A4Linear:
         M = x2.shape[0]
         if self._work is None or self._work[0].shape[0] != M:
             torch = self._torch
+            need = apex4_w4a4_gemm_workspace_size(M, self.N, self.K, self.G) if M else 0
             self._work = (torch.empty((M, self.K // 2), dtype=torch.uint8, device=x2.device),
-                          torch.empty((M, max(self.K // self.G, 1)), dtype=torch.float16, device=x2.device))
-        Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, self._work[0], self._work[1])
+                          torch.empty((M, max(self.K // self.G, 1)), dtype=torch.float16, device=x2.device),
+                          torch.empty((need,), dtype=torch.uint8, device=x2.device) if need else None)
+        Aq, sa, ws = self._work
+        if ws is None:
+            Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, Aq, sa)
+        else:
+            apex4_quantize_act(x2, self.G, Aq, sa)
+            Y = apex4_w4a4_gemm_ws(Aq, sa, self.W_q, self.s_w, self.G, ws)
         return Y.reshape(*lead, self.N)

@@ -17,6 +17,17 @@ hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                        const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
                        uint16_t* Y, int32_t* P, hipStream_t stream);
 
+// G = 128 GEMM split over K across workgroups for shapes whose 128 x 256 tiles
+// leave CUs idle: S fp32 partial planes part[S][M][N] (caller workspace of
+// splitk_workspace_bytes bytes), summed in split order and rounded once.
+// splitk_factor() == 1 (workspace 0) where no split applies; launch_gemm_splitk
+// then runs launch_gemm.
+int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G);
+int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G);
+hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
+                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
+                              hipStream_t stream);
+
 // Compute units of the current device (cached after the first call).
 int device_cu_count();
 

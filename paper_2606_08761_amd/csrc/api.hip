@@ -86,6 +86,7 @@ const char* apex4_status_string(int status) {
         case APEX4_ERR_ALIGN: return "APEX4_ERR_ALIGN: a pointer is not 16-byte aligned";
         case APEX4_ERR_LAUNCH: return "APEX4_ERR_LAUNCH: kernel launch failed";
         case APEX4_ERR_DEVICE: return "APEX4_ERR_DEVICE: no gfx950 device is current";
+        case APEX4_ERR_WORKSPACE: return "APEX4_ERR_WORKSPACE: workspace NULL or too small";
         default: return "APEX4: unknown status";
     }
 }
@@ -114,6 +115,41 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, con
     hipError_t e = apex4::launch_gemm(A_q, static_cast<const uint16_t*>(s_a), W_q,
                                       static_cast<const uint16_t*>(s_w), M, N, K, G, static_cast<uint16_t*>(Y),
                                       nullptr, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int64_t G, int64_t* bytes) {
+    if (!bytes) return APEX4_ERR_NULL;
+    int rc = check_gemm_shape(M, N, K);
+    if (rc) return rc;
+    rc = check_gemm_group(K, G);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    *bytes = apex4::splitk_workspace_bytes(M, N, K, G);
+    return APEX4_OK;
+}
+
+int apex4_w4a4_gemm_ws(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
+                       int64_t N, int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes,
+                       void* stream) {
+    int rc = check_gemm_args(A_q, s_a, W_q, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const int64_t need = apex4::splitk_workspace_bytes(M, N, K, G);
+    hipError_t e;
+    if (need == 0) {
+        e = apex4::launch_gemm(A_q, static_cast<const uint16_t*>(s_a), W_q, static_cast<const uint16_t*>(s_w), M, N,
+                               K, G, static_cast<uint16_t*>(Y), nullptr, static_cast<hipStream_t>(stream));
+    } else {
+        if (!workspace || workspace_bytes < need) return APEX4_ERR_WORKSPACE;
+        e = apex4::launch_gemm_splitk(A_q, static_cast<const uint16_t*>(s_a), W_q, static_cast<const uint16_t*>(s_w),
+                                      M, N, K, G, static_cast<uint16_t*>(Y), static_cast<float*>(workspace),
+                                      static_cast<hipStream_t>(stream));
+    }
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 

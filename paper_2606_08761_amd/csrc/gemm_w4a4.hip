@@ -593,7 +593,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
 //     cover each).
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
-    const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y) {
+    const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y, int nks_split,
+    float* __restrict__ part) {
     constexpr int NT = 512, BM = 128, BN = 256, MI = 4;
     __shared__ Stage<BM, NT, 1> st[2];
 
@@ -620,7 +621,9 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const bool grp_y = wave >= 4;  // uniform per wave
     const int l32 = lane & 31, lh = lane >> 5;
-    const int nks = K / KS;
+    // K range: stages [kofs, kofs + nks) of this workgroup's split (blockIdx.y)
+    const int nks = nks_split;
+    const int kofs = static_cast<int>(blockIdx.y) * nks_split;
     const int ng = K / 128;
 
     // this thread's 16-byte chunk of A per stage and its widened LDS places
@@ -639,7 +642,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     uint16_t rsc;
     uint4 w[2];
     auto load_a = [&](int ks) __attribute__((always_inline)) {
-        ks = min(ks, nks - 1);
+        ks = min(ks, nks - 1) + kofs;
         ra = *reinterpret_cast<const uint4*>(Aq + static_cast<int64_t>(ks) * (KS / 2) + a_off);
         rsc = sc_base[sc_off + static_cast<uint32_t>(ks)];
     };
@@ -649,7 +652,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
         st[buf].scale[0][tid] = rsc;
     };
     auto load_w = [&](int ks) __attribute__((always_inline)) {
-        ks = min(ks, nks - 1);
+        ks = min(ks, nks - 1) + kofs;
         const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2) + w_off;
         w[0] = *reinterpret_cast<const uint4*>(base);
         w[1] = *reinterpret_cast<const uint4*>(base + 16);
@@ -765,7 +768,30 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     }
     if (!grp_y) __syncthreads();
 
-    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3
+    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3.
+    // Split K: the fp32 partial tile goes to part[split][m][n] instead.
+    if (part) {
+        float* pbase = part + static_cast<int64_t>(blockIdx.y) * M * N;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int gm = m0 + i * 32 + l32;
+            if (gm >= M) continue;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int gn = n0 + wave * 32 + 8 * q + 4 * lh;
+                float* dst = pbase + static_cast<int64_t>(gm) * N + gn;
+                if ((N & 3) == 0 && gn + 3 < N) {
+                    *reinterpret_cast<float4*>(dst) =
+                        make_float4(acc[i][4 * q], acc[i][4 * q + 1], acc[i][4 * q + 2], acc[i][4 * q + 3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (gn + e < N) dst[e] = acc[i][4 * q + e];
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         const int gm = m0 + i * 32 + l32;
@@ -853,13 +879,91 @@ hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq
             const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
             if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
             hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, Aq, sa, Wq,
-                               sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+                               sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
+                               static_cast<int>(K / KS), static_cast<float*>(nullptr));
             return hipGetLastError();
         }
         return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     }
     if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+}
+
+namespace {
+
+// Y = binary16(part[0] + part[1] + ... + part[S-1]), summed in split order:
+// four elements per thread when M N is a multiple of 4 (16-byte aligned
+// partial planes), one otherwise.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int S, int64_t MN,
+                                                            uint16_t* __restrict__ Y) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    if ((MN & 3) == 0) {
+        for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < MN / 4; i += stride) {
+            float4 a = reinterpret_cast<const float4*>(part)[i];
+            for (int sp = 1; sp < S; ++sp) {
+                const float4 b = reinterpret_cast<const float4*>(part + sp * MN)[i];
+                a.x += b.x;
+                a.y += b.y;
+                a.z += b.z;
+                a.w += b.w;
+            }
+            const uint32_t lo = __half_as_ushort(__float2half_rn(a.x)) |
+                                (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(a.y))) << 16);
+            const uint32_t hi = __half_as_ushort(__float2half_rn(a.z)) |
+                                (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(a.w))) << 16);
+            reinterpret_cast<uint2*>(Y)[i] = make_uint2(lo, hi);
+        }
+    } else {
+        for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < MN; i += stride) {
+            float a = part[i];
+            for (int sp = 1; sp < S; ++sp) a += part[sp * MN + i];
+            Y[i] = __half_as_ushort(__float2half_rn(a));
+        }
+    }
+}
+
+}  // namespace
+
+// Split factor for the G = 128 tile kernel when it leaves CUs idle: the
+// largest S in {2, 4, 8} with tiles * S <= CUs, S dividing the stage count and
+// at least 4 stages per split; 1 where no split applies.  S = 2 is taken only
+// from M = 256 on: below that the 128-row tiles are half empty and the
+// 64 x 128 tiles of launch_gemm, which already fill the CUs, were faster
+// (MI355X, M = 64, N = 28672, K = 8192: 39.5 us against 49.6 us split).
+int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G) {
+    if (G != 128 || M <= 0 || gemv_fits(M, N, K, G) || decode_fits(M, N, K, G)) return 1;
+    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    const int64_t cus = device_cu_count();
+    if (tiles >= cus) return 1;
+    const int64_t nks = K / KS;
+    int S = 1;
+    for (int c = 2; c <= 8; c *= 2)
+        if (tiles * c <= cus && nks % c == 0 && nks / c >= 4) S = c;
+    return (S == 2 && M < 256) ? 1 : S;
+}
+
+int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G) {
+    const int S = splitk_factor(M, N, K, G);
+    return S > 1 ? static_cast<int64_t>(S) * M * N * static_cast<int64_t>(sizeof(float)) : 0;
+}
+
+hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
+                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
+                              hipStream_t stream) {
+    const int S = splitk_factor(M, N, K, G);
+    if (S < 2) return launch_gemm(Aq, sa, Wq, sw, M, N, K, G, Y, nullptr, stream);
+    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(512), 0,
+                       stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
+                       static_cast<int>(K / KS / S), part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t MN = M * N;
+    const int64_t items = (MN & 3) == 0 ? MN / 4 : MN;
+    const int64_t need = (items + 255) / 256;
+    const int blocks = static_cast<int>(need < 8192 ? need : 8192);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, stream, part, S, MN, Y);
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,

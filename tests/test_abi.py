@@ -36,8 +36,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-              "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_status_string",
-              "apex4_version"):
+              "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
+              "apex4_w4a4_gemm_ws", "apex4_status_string", "apex4_version"):
         assert f in names
 
 
@@ -55,6 +55,7 @@ def test_status_strings(L):
     for code, name in {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
                        -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}.items():
         assert L.apex4_status_string(code).decode().startswith(name)
+    assert L.apex4_status_string(-7).decode().startswith("APEX4_ERR_WORKSPACE")
     assert L.apex4_status_string(12345)
     assert L.apex4_version() >= 100
 
@@ -159,6 +160,23 @@ def test_fp6_validation(L):
     assert g(*ok, 1 << 20, 8, 6144, 128, h.ptr(), s) == -2         # A_6 of 4.5 GiB
     assert g(*ok, 4, 1 << 21, 4096, 128, h.ptr(), s) == -2         # W_6 of 6 GiB
     assert g(h.ptr(4), *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -4
+
+
+def test_workspace_validation(L):
+    h = Host()
+    q = L.apex4_w4a4_gemm_workspace_size
+    b = ctypes.c_int64(-1)
+    assert q(4, 8, 256, 128, None) == -1
+    assert q(4, 8, 200, 128, ctypes.byref(b)) == -2
+    assert q(4, 8, 384, 96, ctypes.byref(b)) == -3
+    assert b.value == -1                                           # nothing written on failure
+    g = L.apex4_w4a4_gemm_ws
+    s = NULL
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), h.ptr(), 1 << 20, s) == -1
+    assert g(*ok, 4, 8, 320, 128, h.ptr(), h.ptr(), 1 << 20, s) == -2
+    assert g(*ok, 4, 8, 256, 96, h.ptr(), h.ptr(), 1 << 20, s) == -3
+    assert g(*ok, 4, 8, 256, 128, h.ptr(), h.ptr(8), 1 << 20, s) == -4   # misaligned workspace
 
 
 def test_device_check_without_gpu():

@@ -322,19 +322,22 @@ def test_w4a4_linear_module(O):
     import torch
     m = pk()
     N, K, G = 1024, 2048, 128
-    x, w = wl.float_workload("tiny", 24, N, K)
+    x, w = wl.float_workload("tiny", 64, N, K)
     lin = m.W4A4Linear(dev(w), G)
     Wq_o, sw_o = O.quantize(w, G)
     assert np.array_equal(host(lin.W_q), Wq_o)
-    for rows in (24, 24, 7):                      # same shape twice (buffers reused), then another
+    # same shape twice (buffers reused), then others; 64 rows take the split-K
+    # GEMM with the layer's own workspace
+    for rows in (24, 24, 7, 64):
         xb = x[:rows]
         y = host(lin(dev(xb).reshape(1, rows, K)))
         assert y.shape == (1, rows, N)
+        assert (lin._work[2] is not None) == (rows == 64)
         Aq_o, sa_o = O.quantize(xb, G)
         check_tolerance(y[0], O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"module rows={rows}")
     # per-channel weights through the same layer
     lin_c = m.W4A4Linear(dev(w), 0)
     Wq_c, sw_c = O.quantize(w, K)
-    Aq_c, sa_c = O.quantize(x, K)
-    check_tolerance(host(lin_c(dev(x))), O.gemm_rows(Aq_c, sa_c, Wq_c, sw_c, K, K), "module per-channel")
+    Aq_c, sa_c = O.quantize(x[:24], K)
+    check_tolerance(host(lin_c(dev(x[:24]))), O.gemm_rows(Aq_c, sa_c, Wq_c, sw_c, K, K), "module per-channel")
     torch.cuda.synchronize()
