@@ -869,6 +869,39 @@ def main():
            "mfma": "v_mfma_scale_f32_32x32x64_f8f6f4, FP6 e3m2 operands, unit E8M0 scales"}
     del c, Yc, A6, W6, Y6
 
+    # ---- MX variant: power-of-two group scales applied inside the FP6 MFMA ----
+    # (a different quantization: its accuracy cost is reported next to the
+    # fp16-scale path's, both against an fp32 GEMM of the unquantized inputs)
+    xm, w16 = sets[0]["x"], torch.from_numpy(w_h).to(dev)
+    A6m, eam = pk.apex4_quantize_mx(xm, G)
+    W6m, ewm = pk.apex4_quantize_mx(w16, G)
+    Ym = torch.empty((M, N), dtype=torch.float16, device=dev)
+    for _ in range(5):
+        pk.apex4_w4a4_gemm_mx(A6m, eam, W6m, ewm, G, Ym)
+    e0.record(stream)
+    for _ in range(reps):
+        pk.apex4_w4a4_gemm_mx(A6m, eam, W6m, ewm, G, Ym)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mx_ms = e0.elapsed_time(e1) / reps
+    e0.record(stream)
+    for _ in range(reps):
+        pk.apex4_quantize_mx(xm, G, A6m, eam)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mxq_ms = e0.elapsed_time(e1) / reps
+    ref = xm.float() @ w16.float().t()
+    rms = lambda t: float(t.double().pow(2).mean().sqrt())
+    pk.apex4_quantize_act(xm, G, sets[0]["Aq"], sets[0]["sa"])
+    pk.apex4_w4a4_gemm(sets[0]["Aq"], sets[0]["sa"], sets[0]["Wq"], sets[0]["sw"], G, sets[0]["Y"])
+    mx = {"gemm_us": round(mx_ms * 1e3, 3), "tops": round(2.0 * M * N * K / (mx_ms * 1e-3) / 1e12, 2),
+          "time_vs_fp16_scale_kernel": round(mx_ms / codes_gemm_ms, 3), "quantize_us": round(mxq_ms * 1e3, 3),
+          "rel_rms_err_vs_fp32": round(rms(Ym.float() - ref) / rms(ref), 5),
+          "fp16_scale_rel_rms_err_vs_fp32": round(rms(sets[0]["Y"].float() - ref) / rms(ref), 5),
+          "scales": "E8M0 powers of two (smallest covering max|x|/7), not the paper's fp16 scales",
+          "mfma": "v_mfma_scale_f32_32x32x64_f8f6f4, FP6 e3m2 codes, per-lane E8M0 group scales"}
+    del A6m, W6m, Ym, ref, w16
+
     # ---- fp16 GEMM of the same shape (torch -> hipBLASLt), rotated too ----
     fsets = []
     Rf = max(2, -(-ROTATE_BYTES // (M * K * 2 + N * K * 2 + M * N * 2)))
@@ -922,6 +955,7 @@ def main():
         "speedup_gemm_vs_fp16": round(fp16_ms / gemm_ms, 3),
         "speedup_step_vs_fp16": round(fp16_ms / ms_per_step, 3),
         "fp6_variant": fp6,
+        "mx_variant": mx,
     }
     if not args.no_decode:
         line["decode"] = decode_bench()

@@ -180,6 +180,31 @@ int apex4_w4a4_gemm_fp6(const uint8_t* A_6, const void* s_a,
                         int64_t M, int64_t N, int64_t K, int64_t G,
                         void* Y, void* stream);
 
+/*
+ * MX numerics variant (CDNA4 only).  NOT the paper's scales: SymQuant's 4-bit
+ * symmetric codes (Sec. 3.2.1) with each group scale restricted to a power of
+ * two, 2^E with E = min{e integer : max|X_g| <= 7 * 2^e} (E = 0 for an all-zero
+ * group), so that the block-scaled FP6 MFMA applies it and no per-group
+ * dequantization is left (Sec. 2.2 makes this point for block-scaled FP4).
+ *
+ * apex4_quantize_mx: x [M, K] binary16 -> Q6 [M, 3K/4] FP6 e3m2 codes (layout
+ *   of apex4_pack_fp6), codes clamp(round-half-even(x / 2^E), -8, 7); e [M, K/G]
+ *   E8M0 bytes E + 127.  Bit-exact and deterministic.
+ * apex4_w4a4_gemm_mx: Y[m,n] = binary16( sum_g 2^(Ea[m,g] + Ew[n,g] - 254) P[m,n,g] )
+ *   with P the exact group sums of Eq. (group_decomposition); accumulated in
+ *   binary32 by the MFMA across all of K, rounded once to binary16.
+ *   A_6 [M, 3K/4], e_a [M, K/G], W_6 [N, 3K/4], e_w [N, K/G] (device,
+ *   read-only); Y [M, N] binary16 (device, output).
+ * G in {32, 64, 128, 256, 512, 1024} with G <= K (APEX4_ERR_GROUP otherwise);
+ * K % 128 == 0, K % G == 0; FP6 operands under 4 GiB; 16-byte aligned pointers.
+ */
+int apex4_quantize_mx(const void* x, int64_t M, int64_t K, int64_t G,
+                      uint8_t* Q6, uint8_t* e, void* stream);
+int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a,
+                       const uint8_t* W_6, const uint8_t* e_w,
+                       int64_t M, int64_t N, int64_t K, int64_t G,
+                       void* Y, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* apex4_status_string(int status);
 

@@ -66,6 +66,13 @@ def unpack(codes: np.ndarray) -> np.ndarray:
 
 def gemm_mx(Aq, ea, Wq, ew, K: int, G: int, rows=None) -> np.ndarray:
     """Y rows (binary16) of the MX GEMM; rows = None for all of them."""
+    y = gemm_mx_f64(Aq, ea, Wq, ew, K, G, rows)
+    with np.errstate(over="ignore"):      # beyond the binary16 range: +-inf, as the rounding defines
+        return y.astype(np.float16)
+
+
+def gemm_mx_f64(Aq, ea, Wq, ew, K: int, G: int, rows=None) -> np.ndarray:
+    """The binary64 sum of the MX GEMM before its final rounding."""
     A = unpack(np.asarray(Aq))
     W = unpack(np.asarray(Wq))
     if rows is not None:
@@ -76,5 +83,4 @@ def gemm_mx(Aq, ea, Wq, ew, K: int, G: int, rows=None) -> np.ndarray:
         P = A[:, g * G:(g + 1) * G] @ W[:, g * G:(g + 1) * G].T          # exact int64
         s = np.exp2(ea[:, g].astype(np.float64) - 127)[:, None] * np.exp2(ew[:, g].astype(np.float64) - 127)[None, :]
         y += s * P                                                       # each term exact: power of two times integer
-    with np.errstate(over="ignore"):      # beyond the binary16 range: +-inf, as the rounding defines
-        return y.astype(np.float16)
+    return y

@@ -26,7 +26,8 @@ STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
             "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
-            "apex4_w4a4_gemm_ws", "apex4_status_string", "apex4_version")
+            "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_status_string",
+            "apex4_version")
 
 _lib = None
 
@@ -53,10 +54,13 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
     L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
     L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
+    L.apex4_quantize_mx.argtypes = [P, I, I, I, P, P, P]
+    L.apex4_w4a4_gemm_mx.argtypes = [P, P, P, P, I, I, I, I, P, P]
     L.apex4_w4a4_gemm_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear",
-              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws"):
+              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
+              "apex4_quantize_mx", "apex4_w4a4_gemm_mx"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -204,6 +208,34 @@ def apex4_w4a4_gemm_fp6(A_6, s_a, W_6, s_w, G: int, Y=None, stream=None):
                                    _dev(W_6, torch.uint8, "W_6"), _dev(s_w, torch.float16, "s_w"),
                                    M, N, 4 * K34 // 3, G, _dev(Y, torch.float16, "Y"), _stream(A_6, stream))
     _check("apex4_w4a4_gemm_fp6", rc)
+    return Y
+
+
+def apex4_quantize_mx(x, G: int, Q6=None, e=None, stream=None):
+    """MX variant quantizer: x [M, K] float16 -> (FP6 codes uint8 [M, 3K/4], E8M0 scales uint8 [M, K/G])."""
+    import torch
+    M, K = x.shape
+    if Q6 is None:
+        Q6 = torch.empty((M, 3 * K // 4), dtype=torch.uint8, device=x.device)
+    if e is None:
+        e = torch.empty((M, K // G), dtype=torch.uint8, device=x.device)
+    rc = lib().apex4_quantize_mx(_dev(x, torch.float16, "x"), M, K, G, _dev(Q6, torch.uint8, "Q6"),
+                                 _dev(e, torch.uint8, "e"), _stream(x, stream))
+    _check("apex4_quantize_mx", rc)
+    return Q6, e
+
+
+def apex4_w4a4_gemm_mx(A_6, e_a, W_6, e_w, G: int, Y=None, stream=None):
+    """MX variant GEMM: power-of-two group scales applied inside the FP6 MFMA."""
+    import torch
+    M, K34 = A_6.shape
+    N = W_6.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_6.device)
+    rc = lib().apex4_w4a4_gemm_mx(_dev(A_6, torch.uint8, "A_6"), _dev(e_a, torch.uint8, "e_a"),
+                                  _dev(W_6, torch.uint8, "W_6"), _dev(e_w, torch.uint8, "e_w"),
+                                  M, N, 4 * K34 // 3, G, _dev(Y, torch.float16, "Y"), _stream(A_6, stream))
+    _check("apex4_w4a4_gemm_mx", rc)
     return Y
 
 

@@ -59,4 +59,12 @@ hipError_t launch_pack_fp6(const uint8_t* q4, int64_t rows, int64_t K, uint8_t* 
 hipError_t launch_gemm_fp6(const uint8_t* A6, const uint16_t* sa, const uint8_t* W6, const uint16_t* sw, int64_t M,
                            int64_t N, int64_t K, uint16_t* Y, hipStream_t stream);
 
+// MX variant: SymQuant codes with power-of-two (E8M0) group scales, written as
+// FP6 e3m2 codes [rows, 3K/4] and scale bytes [rows, K/G]; and the GEMM that
+// applies the scales inside the block-scaled FP6 MFMA (G in 32..1024).
+hipError_t launch_quant_mx(const uint16_t* x, int64_t M, int64_t K, int64_t G, uint8_t* q6, uint8_t* e,
+                           hipStream_t stream);
+hipError_t launch_gemm_mx(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
+                          int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream);
+
 }  // namespace apex4

@@ -228,4 +228,40 @@ int apex4_w4a4_gemm_fp6(const uint8_t* A_6, const void* s_a, const uint8_t* W_6,
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 
+namespace {
+bool mx_group(int64_t G) { return G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024; }
+}  // namespace
+
+int apex4_quantize_mx(const void* x, int64_t M, int64_t K, int64_t G, uint8_t* Q6, uint8_t* e, void* stream) {
+    if (!present(x, M) || !present(Q6, M) || !present(e, M)) return APEX4_ERR_NULL;
+    if (M < 0 || K < 128 || (K % 128) != 0 || M > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (!mx_group(G) || G > K) return APEX4_ERR_GROUP;
+    if (K % G != 0) return APEX4_ERR_SHAPE;
+    if (!aligned16(x) || !aligned16(Q6) || !aligned16(e)) return APEX4_ERR_ALIGN;
+    const int rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const hipError_t err = apex4::launch_quant_mx(static_cast<const uint16_t*>(x), M, K, G, Q6, e,
+                                                  static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a, const uint8_t* W_6, const uint8_t* e_w, int64_t M,
+                       int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+    if (!present(A_6, M) || !present(e_a, M) || !W_6 || !e_w || !present(Y, M)) return APEX4_ERR_NULL;
+    if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
+    if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (M * (3 * K / 4) > 0xFFFFFFFFll || N * (3 * K / 4) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
+    if (!mx_group(G) || G > K) return APEX4_ERR_GROUP;
+    if (K % G != 0) return APEX4_ERR_SHAPE;
+    if (!aligned16(A_6) || !aligned16(e_a) || !aligned16(W_6) || !aligned16(e_w) || !aligned16(Y))
+        return APEX4_ERR_ALIGN;
+    const int rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const hipError_t err = apex4::launch_gemm_mx(A_6, e_a, W_6, e_w, M, N, K, G, static_cast<uint16_t*>(Y),
+                                                 static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
 }  // extern "C"

@@ -37,7 +37,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
               "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
-              "apex4_w4a4_gemm_ws", "apex4_status_string", "apex4_version"):
+              "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_status_string",
+              "apex4_version"):
         assert f in names
 
 
@@ -177,6 +178,27 @@ def test_workspace_validation(L):
     assert g(*ok, 4, 8, 320, 128, h.ptr(), h.ptr(), 1 << 20, s) == -2
     assert g(*ok, 4, 8, 256, 96, h.ptr(), h.ptr(), 1 << 20, s) == -3
     assert g(*ok, 4, 8, 256, 128, h.ptr(), h.ptr(8), 1 << 20, s) == -4   # misaligned workspace
+
+
+def test_mx_validation(L):
+    h = Host()
+    q = L.apex4_quantize_mx
+    s = NULL
+    assert q(NULL, 4, 256, 128, h.ptr(), h.ptr(), s) == -1
+    assert q(h.ptr(), 4, 200, 128, h.ptr(), h.ptr(), s) == -2       # K % 128
+    assert q(h.ptr(), 4, 256, 96, h.ptr(), h.ptr(), s) == -3        # G not a power of two in 32..1024
+    assert q(h.ptr(), 4, 256, 512, h.ptr(), h.ptr(), s) == -3       # G > K
+    assert q(h.ptr(), 4, 256, 2048, h.ptr(), h.ptr(), s) == -3
+    assert q(h.ptr(), 4, 384, 256, h.ptr(), h.ptr(), s) == -2       # K % G
+    assert q(h.ptr(4), 4, 256, 128, h.ptr(), h.ptr(), s) == -4
+    g = L.apex4_w4a4_gemm_mx
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -1
+    assert g(*ok, 4, 8, 256, 128, NULL, s) == -1
+    assert g(*ok, 4, 0, 256, 128, h.ptr(), s) == -2
+    assert g(*ok, 4, 8, 256, 48, h.ptr(), s) == -3
+    assert g(*ok, 1 << 20, 8, 6144, 128, h.ptr(), s) == -2          # A_6 of 4.5 GiB
+    assert g(*ok, 4, 8, 256, 128, h.ptr(2), s) == -4
 
 
 def test_device_check_without_gpu():
