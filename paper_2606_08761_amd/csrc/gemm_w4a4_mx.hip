@@ -99,10 +99,11 @@ __global__ __launch_bounds__(256) void quant_mx_kernel(const uint16_t* __restric
     if (blk % B == 0) e[row * (bpr / B) + blk / B] = static_cast<uint8_t>(E + 127);
 }
 
+template <int BM>
 struct StageMX {
-    uint8_t a[128 * MX_LROW];
+    uint8_t a[BM * MX_LROW];
     uint8_t w[256 * MX_LROW];
-    uint32_t sa[128];  // four block scales (bytes 0..3 = blocks 0..3 of the stage) per activation row
+    uint32_t sa[BM];   // four block scales (bytes 0..3 = blocks 0..3 of the stage) per activation row
     uint32_t sw[256];  // the same per weight row
 };
 
@@ -138,12 +139,16 @@ __device__ __forceinline__ uint32_t expand_scales(uint32_t v) {
     }
 }
 
-template <int GB>
+// WM = 1: 128 x 256 tiles, 8 waves of 128 x 32; WM = 2: 256 x 256 tiles, 2 x 4
+// waves of 128 x 64 (two column blocks per wave share each activation
+// fragment: 40 % fewer LDS bytes per MFMA, half the staging per output).
+template <int GB, int WM>
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
     const uint8_t* __restrict__ A6, const uint8_t* __restrict__ ea, const uint8_t* __restrict__ W6,
     const uint8_t* __restrict__ ew, int M, int N, int K, uint16_t* __restrict__ Y) {
-    constexpr int BM = 128, BN = 256, MI = 4;
-    __shared__ StageMX st[2];
+    constexpr int BM = 128 * WM, BN = 256, MI = 4, NJ = WM, WN = 8 / WM;
+    constexpr int ACH = (BM * 6 + 511) / 512;  // 16-byte activation chunks per thread and stage
+    __shared__ StageMX<BM> st[2];
 
     // tile selection (XCD-aware, as the other tile kernels)
     const int mt_count = (M + BM - 1) / BM;
@@ -166,33 +171,36 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int wm = wave / WN, wn = wave % WN;
     const int l32 = lane & 31, lh = lane >> 5;
     const int nks = K / 128;
     const uint32_t rowb = static_cast<uint32_t>(3 * K / 4);
     const int ng = K / (32 * GB);
 
-    // staging, per stage: activations 768 chunks of 16 bytes (waves 0-3 take two,
-    // 4-7 one), weights 1536 (three per thread), scales one row per thread < 384
+    // staging, per stage: activations BM * 6 chunks of 16 bytes (chunk tid + 512 i:
+    // row c / 6, byte 16 (c % 6); with WM = 1 waves 0-3 take two and 4-7 one),
+    // weights 1536 (three per thread), scales one row per thread below BM + 256.
+    // Offsets are kept in scalars, not arrays, which the compiler would move to LDS.
     auto a_g = [&](int c) { return static_cast<uint32_t>(min(m0 + c / 6, M - 1)) * rowb + 16 * (c % 6); };
-    auto a_l = [&](int c) { return (c / 6) * MX_LROW + 16 * (c % 6); };
     auto w_g = [&](int c) { return static_cast<uint32_t>(min(n0 + c / 6, N - 1)) * rowb + 16 * (c % 6); };
-    auto w_l = [&](int c) { return (c / 6) * MX_LROW + 16 * (c % 6); };
-    const bool two_a = tid < 256;
-    const uint32_t ag0 = a_g(tid), ag1 = a_g(two_a ? tid + 512 : tid);
-    const int al0 = a_l(tid), al1 = a_l(two_a ? tid + 512 : tid);
+    auto l_of = [&](int c) { return (c / 6) * MX_LROW + 16 * (c % 6); };
+    const bool a1 = tid + 512 < BM * 6, a2 = ACH > 2 && tid + 1024 < BM * 6;
+    const uint32_t ag0 = a_g(tid), ag1 = a_g(a1 ? tid + 512 : tid), ag2 = a_g(a2 ? tid + 1024 : tid);
+    const int al0 = l_of(tid), al1 = l_of(a1 ? tid + 512 : tid), al2 = l_of(a2 ? tid + 1024 : tid);
     const uint32_t wg0 = w_g(tid), wg1 = w_g(tid + 512), wg2 = w_g(tid + 1024);
-    const int wl0 = w_l(tid), wl1 = w_l(tid + 512), wl2 = w_l(tid + 1024);
+    const int wl0 = l_of(tid), wl1 = l_of(tid + 512), wl2 = l_of(tid + 1024);
     const bool sc_a = tid < BM, sc_w = tid >= BM && tid < BM + BN;
     const uint8_t* erow = sc_a ? ea + static_cast<int64_t>(min(m0 + tid, M - 1)) * ng
                                : ew + static_cast<int64_t>(min(n0 + min(tid - BM, BN - 1), N - 1)) * ng;
 
-    uint4 ra0, ra1, rw0, rw1, rw2;
+    uint4 ra0, ra1, ra2, rw0, rw1, rw2;
     uint32_t rsc = 0;
     auto load = [&](int s) __attribute__((always_inline)) {
         s = min(s, nks - 1);
         const uint8_t* abase = A6 + static_cast<int64_t>(s) * MX_SROW;
         ra0 = *reinterpret_cast<const uint4*>(abase + ag0);
-        if (two_a) ra1 = *reinterpret_cast<const uint4*>(abase + ag1);
+        if (a1) ra1 = *reinterpret_cast<const uint4*>(abase + ag1);
+        if (a2) ra2 = *reinterpret_cast<const uint4*>(abase + ag2);
         const uint8_t* wbase = W6 + static_cast<int64_t>(s) * MX_SROW;
         rw0 = *reinterpret_cast<const uint4*>(wbase + wg0);
         rw1 = *reinterpret_cast<const uint4*>(wbase + wg1);
@@ -201,7 +209,8 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
     };
     auto store = [&](int buf) __attribute__((always_inline)) {
         *reinterpret_cast<uint4*>(&st[buf].a[al0]) = ra0;
-        if (two_a) *reinterpret_cast<uint4*>(&st[buf].a[al1]) = ra1;
+        if (a1) *reinterpret_cast<uint4*>(&st[buf].a[al1]) = ra1;
+        if (a2) *reinterpret_cast<uint4*>(&st[buf].a[al2]) = ra2;
         *reinterpret_cast<uint4*>(&st[buf].w[wl0]) = rw0;
         *reinterpret_cast<uint4*>(&st[buf].w[wl1]) = rw1;
         *reinterpret_cast<uint4*>(&st[buf].w[wl2]) = rw2;
@@ -225,24 +234,31 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
         return o;
     };
 
-    f32x16 D[MI];
+    f32x16 D[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) D[i][r] = 0.f;
+        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) D[i][j][r] = 0.f;
 
     auto compute = [&](int buf) __attribute__((always_inline)) {
-        uint4 wf[3], af[2][3];
-        const uint8_t* wp = &st[buf].w[(wave * 32 + l32) * MX_LROW + 48 * lh];
+        uint4 wf[NJ][3], af[2][3];
+        int scw[NJ];
 #pragma unroll
-        for (int q = 0; q < 3; ++q) wf[q] = *reinterpret_cast<const uint4*>(wp + 16 * q);
-        // this lane's two block scales (kk = 0, 1) in bytes 0 and 1
-        const int scw = static_cast<int>(st[buf].sw[wave * 32 + l32] >> (16 * lh));
+        for (int j = 0; j < NJ; ++j) {
+            const int wr = wn * 32 * NJ + j * 32 + l32;
+            const uint8_t* wp = &st[buf].w[wr * MX_LROW + 48 * lh];
+#pragma unroll
+            for (int q = 0; q < 3; ++q) wf[j][q] = *reinterpret_cast<const uint4*>(wp + 16 * q);
+            // this lane's two block scales (kk = 0, 1) in bytes 0 and 1
+            scw[j] = static_cast<int>(st[buf].sw[wr] >> (16 * lh));
+        }
         int sca[MI];
 #pragma unroll
-        for (int i = 0; i < MI; ++i) sca[i] = static_cast<int>(st[buf].sa[i * 32 + l32] >> (16 * lh));
+        for (int i = 0; i < MI; ++i) sca[i] = static_cast<int>(st[buf].sa[wm * 128 + i * 32 + l32] >> (16 * lh));
         auto frag = [&](int i, uint4 (&f)[3]) __attribute__((always_inline)) {
-            const uint8_t* p = &st[buf].a[(i * 32 + l32) * MX_LROW + 48 * lh];
+            const uint8_t* p = &st[buf].a[(wm * 128 + i * 32 + l32) * MX_LROW + 48 * lh];
 #pragma unroll
             for (int q = 0; q < 3; ++q) f[q] = *reinterpret_cast<const uint4*>(p + 16 * q);
         };
@@ -250,10 +266,13 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
         static_for_mx<MI>([&](auto II) __attribute__((always_inline)) {
             constexpr int i = decltype(II)::value;
             if constexpr (i + 1 < MI) frag(i + 1, af[(i + 1) & 1]);
-            D[i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(operand(wf, 0), operand(af[i & 1], 0), D[i],
-                                                                   MX_FMT, MX_FMT, 0, scw, 0, sca[i]);
-            D[i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(operand(wf, 1), operand(af[i & 1], 1), D[i],
-                                                                   MX_FMT, MX_FMT, 1, scw, 1, sca[i]);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                D[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                    operand(wf[j], 0), operand(af[i & 1], 0), D[i][j], MX_FMT, MX_FMT, 0, scw[j], 0, sca[i]);
+                D[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                    operand(wf[j], 1), operand(af[i & 1], 1), D[i][j], MX_FMT, MX_FMT, 1, scw[j], 1, sca[i]);
+            }
         });
     };
 
@@ -271,26 +290,29 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
         __syncthreads();
     }
 
-    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3
+    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3, of each block
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-        const int gm = m0 + i * 32 + l32;
+        const int gm = m0 + wm * 128 + i * 32 + l32;
         if (gm >= M) continue;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const uint32_t h01 = __half_as_ushort(__float2half_rn(D[i][4 * q + 0])) |
-                                 (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(D[i][4 * q + 1]))) << 16);
-            const uint32_t h23 = __half_as_ushort(__float2half_rn(D[i][4 * q + 2])) |
-                                 (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(D[i][4 * q + 3]))) << 16);
-            const int gn = n0 + wave * 32 + 8 * q + 4 * lh;
-            uint16_t* dst = Y + static_cast<int64_t>(gm) * N + gn;
-            if ((N & 3) == 0 && gn + 3 < N) {
-                *reinterpret_cast<uint2*>(dst) = make_uint2(h01, h23);
-            } else {
-                if (gn + 0 < N) dst[0] = static_cast<uint16_t>(h01 & 0xFFFFu);
-                if (gn + 1 < N) dst[1] = static_cast<uint16_t>(h01 >> 16);
-                if (gn + 2 < N) dst[2] = static_cast<uint16_t>(h23 & 0xFFFFu);
-                if (gn + 3 < N) dst[3] = static_cast<uint16_t>(h23 >> 16);
+        for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t h01 = __half_as_ushort(__float2half_rn(D[i][j][4 * q + 0])) |
+                                     (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(D[i][j][4 * q + 1]))) << 16);
+                const uint32_t h23 = __half_as_ushort(__float2half_rn(D[i][j][4 * q + 2])) |
+                                     (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(D[i][j][4 * q + 3]))) << 16);
+                const int gn = n0 + wn * 32 * NJ + j * 32 + 8 * q + 4 * lh;
+                uint16_t* dst = Y + static_cast<int64_t>(gm) * N + gn;
+                if ((N & 3) == 0 && gn + 3 < N) {
+                    *reinterpret_cast<uint2*>(dst) = make_uint2(h01, h23);
+                } else {
+                    if (gn + 0 < N) dst[0] = static_cast<uint16_t>(h01 & 0xFFFFu);
+                    if (gn + 1 < N) dst[1] = static_cast<uint16_t>(h01 >> 16);
+                    if (gn + 2 < N) dst[2] = static_cast<uint16_t>(h23 & 0xFFFFu);
+                    if (gn + 3 < N) dst[3] = static_cast<uint16_t>(h23 >> 16);
+                }
             }
         }
     }
@@ -309,10 +331,18 @@ hipError_t launch_quant_mx_b(const uint16_t* x, int64_t M, int64_t K, uint8_t* q
 template <int GB>
 hipError_t launch_gemm_mx_g(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
                             int64_t N, int64_t K, uint16_t* Y, hipStream_t stream) {
+    // 256-row tiles where they still give every CU a workgroup
+    const int64_t big = ((M + 255) / 256) * ((N + 255) / 256);
+    if (big >= device_cu_count()) {
+        if (big > 0x7FFFFFFF) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((w4a4_gemm_mx_kernel<GB, 2>), dim3(static_cast<unsigned>(big)), dim3(512), 0, stream, A6, ea,
+                           W6, ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+        return hipGetLastError();
+    }
     const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(w4a4_gemm_mx_kernel<GB>, dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, A6, ea, W6,
-                       ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+    hipLaunchKernelGGL((w4a4_gemm_mx_kernel<GB, 1>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, A6, ea,
+                       W6, ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
     return hipGetLastError();
 }
 
