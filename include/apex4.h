@@ -205,6 +205,22 @@ int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a,
                        int64_t M, int64_t N, int64_t K, int64_t G,
                        void* Y, void* stream);
 
+/*
+ * Workspace form of apex4_w4a4_gemm_mx, as apex4_w4a4_gemm_ws is of
+ * apex4_w4a4_gemm: when the MX GEMM's tiles leave compute units idle, K is
+ * split into S in {2, 4, 8} ranges; fp32 partial tiles go to the caller's
+ * workspace (S * M * N * 4 bytes, from the size query; 0 = no split, then this
+ * is apex4_w4a4_gemm_mx and workspace may be NULL) and are summed in range
+ * order, then rounded once to binary16.  Deterministic, within the tolerance
+ * of the unsplit result.  Errors as apex4_w4a4_gemm_mx, plus
+ * APEX4_ERR_WORKSPACE (checked last, after the device).
+ */
+int apex4_w4a4_gemm_mx_workspace_size(int64_t M, int64_t N, int64_t K, int64_t G, int64_t* bytes);
+int apex4_w4a4_gemm_mx_ws(const uint8_t* A_6, const uint8_t* e_a,
+                          const uint8_t* W_6, const uint8_t* e_w,
+                          int64_t M, int64_t N, int64_t K, int64_t G,
+                          void* Y, void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* apex4_status_string(int status);
 

@@ -26,8 +26,8 @@ STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
             "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
-            "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_status_string",
-            "apex4_version")
+            "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
+            "apex4_w4a4_gemm_mx_ws", "apex4_status_string", "apex4_version")
 
 _lib = None
 
@@ -56,11 +56,14 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
     L.apex4_quantize_mx.argtypes = [P, I, I, I, P, P, P]
     L.apex4_w4a4_gemm_mx.argtypes = [P, P, P, P, I, I, I, I, P, P]
+    L.apex4_w4a4_gemm_mx_workspace_size.argtypes = [I, I, I, I, P]
+    L.apex4_w4a4_gemm_mx_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear",
               "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
-              "apex4_quantize_mx", "apex4_w4a4_gemm_mx"):
+              "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
+              "apex4_w4a4_gemm_mx_ws"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -236,6 +239,31 @@ def apex4_w4a4_gemm_mx(A_6, e_a, W_6, e_w, G: int, Y=None, stream=None):
                                   _dev(W_6, torch.uint8, "W_6"), _dev(e_w, torch.uint8, "e_w"),
                                   M, N, 4 * K34 // 3, G, _dev(Y, torch.float16, "Y"), _stream(A_6, stream))
     _check("apex4_w4a4_gemm_mx", rc)
+    return Y
+
+
+def apex4_w4a4_gemm_mx_workspace_size(M: int, N: int, K: int, G: int) -> int:
+    """Bytes of workspace apex4_w4a4_gemm_mx_ws needs for this shape on the current device (0: none)."""
+    b = ctypes.c_int64(0)
+    _check("apex4_w4a4_gemm_mx_workspace_size", lib().apex4_w4a4_gemm_mx_workspace_size(M, N, K, G, ctypes.byref(b)))
+    return int(b.value)
+
+
+def apex4_w4a4_gemm_mx_ws(A_6, e_a, W_6, e_w, G: int, workspace=None, Y=None, stream=None):
+    """apex4_w4a4_gemm_mx split over K when its tiles leave CUs idle (workspace made here when None)."""
+    import torch
+    M, K34 = A_6.shape
+    N, K = W_6.shape[0], 4 * K34 // 3
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_6.device)
+    if workspace is None:
+        need = apex4_w4a4_gemm_mx_workspace_size(M, N, K, G)
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=A_6.device)
+    rc = lib().apex4_w4a4_gemm_mx_ws(_dev(A_6, torch.uint8, "A_6"), _dev(e_a, torch.uint8, "e_a"),
+                                     _dev(W_6, torch.uint8, "W_6"), _dev(e_w, torch.uint8, "e_w"), M, N, K, G,
+                                     _dev(Y, torch.float16, "Y"), _dev(workspace, torch.uint8, "workspace"),
+                                     workspace.numel(), _stream(A_6, stream))
+    _check("apex4_w4a4_gemm_mx_ws", rc)
     return Y
 
 

@@ -28,6 +28,9 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
                               hipStream_t stream);
 
+// Y = binary16(sum of the S fp32 planes part[S][M N]) in plane order.
+hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* Y, hipStream_t stream);
+
 // Compute units of the current device (cached after the first call).
 int device_cu_count();
 
@@ -66,5 +69,12 @@ hipError_t launch_quant_mx(const uint16_t* x, int64_t M, int64_t K, int64_t G, u
                            hipStream_t stream);
 hipError_t launch_gemm_mx(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
                           int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream);
+// The MX GEMM split over K across workgroups when its tiles leave CUs idle:
+// fp32 partial planes in a caller workspace of mx_splitk_workspace_bytes
+// (0: no split; launch_gemm_mx_splitk then runs launch_gemm_mx).
+int64_t mx_splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G);
+hipError_t launch_gemm_mx_splitk(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew,
+                                 int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
+                                 hipStream_t stream);
 
 }  // namespace apex4

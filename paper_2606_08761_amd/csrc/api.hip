@@ -246,8 +246,8 @@ int apex4_quantize_mx(const void* x, int64_t M, int64_t K, int64_t G, uint8_t* Q
     return err == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 
-int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a, const uint8_t* W_6, const uint8_t* e_w, int64_t M,
-                       int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+int check_mx_gemm_args(const void* A_6, const void* e_a, const void* W_6, const void* e_w, int64_t M, int64_t N,
+                       int64_t K, int64_t G, const void* Y) {
     if (!present(A_6, M) || !present(e_a, M) || !W_6 || !e_w || !present(Y, M)) return APEX4_ERR_NULL;
     if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
     if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
@@ -256,11 +256,49 @@ int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a, const uint8_t* W_
     if (K % G != 0) return APEX4_ERR_SHAPE;
     if (!aligned16(A_6) || !aligned16(e_a) || !aligned16(W_6) || !aligned16(e_w) || !aligned16(Y))
         return APEX4_ERR_ALIGN;
-    const int rc = check_device();
+    return APEX4_OK;
+}
+
+int apex4_w4a4_gemm_mx(const uint8_t* A_6, const uint8_t* e_a, const uint8_t* W_6, const uint8_t* e_w, int64_t M,
+                       int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+    int rc = check_mx_gemm_args(A_6, e_a, W_6, e_w, M, N, K, G, Y);
+    if (rc) return rc;
+    rc = check_device();
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
     const hipError_t err = apex4::launch_gemm_mx(A_6, e_a, W_6, e_w, M, N, K, G, static_cast<uint16_t*>(Y),
                                                  static_cast<hipStream_t>(stream));
+    return err == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_mx_workspace_size(int64_t M, int64_t N, int64_t K, int64_t G, int64_t* bytes) {
+    if (!bytes) return APEX4_ERR_NULL;
+    if (M < 0 || N < 1 || K < 128 || (K % 128) != 0 || M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF)
+        return APEX4_ERR_SHAPE;
+    if (!mx_group(G) || G > K) return APEX4_ERR_GROUP;
+    if (K % G != 0) return APEX4_ERR_SHAPE;
+    const int rc = check_device();
+    if (rc) return rc;
+    *bytes = apex4::mx_splitk_workspace_bytes(M, N, K, G);
+    return APEX4_OK;
+}
+
+int apex4_w4a4_gemm_mx_ws(const uint8_t* A_6, const uint8_t* e_a, const uint8_t* W_6, const uint8_t* e_w, int64_t M,
+                          int64_t N, int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes,
+                          void* stream) {
+    int rc = check_mx_gemm_args(A_6, e_a, W_6, e_w, M, N, K, G, Y);
+    if (rc) return rc;
+    if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const int64_t need = apex4::mx_splitk_workspace_bytes(M, N, K, G);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return APEX4_ERR_WORKSPACE;
+    const hipError_t err =
+        need == 0 ? apex4::launch_gemm_mx(A_6, e_a, W_6, e_w, M, N, K, G, static_cast<uint16_t*>(Y),
+                                          static_cast<hipStream_t>(stream))
+                  : apex4::launch_gemm_mx_splitk(A_6, e_a, W_6, e_w, M, N, K, G, static_cast<uint16_t*>(Y),
+                                                 static_cast<float*>(workspace), static_cast<hipStream_t>(stream));
     return err == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 

@@ -947,6 +947,14 @@ int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G) {
     return S > 1 ? static_cast<int64_t>(S) * M * N * static_cast<int64_t>(sizeof(float)) : 0;
 }
 
+hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* Y, hipStream_t stream) {
+    const int64_t items = (MN & 3) == 0 ? MN / 4 : MN;
+    const int64_t need = (items + 255) / 256;
+    const int blocks = static_cast<int>(need < 8192 ? need : 8192);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, stream, part, S, MN, Y);
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
                               hipStream_t stream) {
@@ -956,14 +964,9 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
     hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(512), 0,
                        stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
                        static_cast<int>(K / KS / S), part);
-    hipError_t e = hipGetLastError();
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t MN = M * N;
-    const int64_t items = (MN & 3) == 0 ? MN / 4 : MN;
-    const int64_t need = (items + 255) / 256;
-    const int blocks = static_cast<int>(need < 8192 ? need : 8192);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, stream, part, S, MN, Y);
-    return hipGetLastError();
+    return launch_splitk_reduce(part, S, M * N, Y, stream);
 }
 
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,

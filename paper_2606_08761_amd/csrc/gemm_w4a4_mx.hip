@@ -145,7 +145,8 @@ __device__ __forceinline__ uint32_t expand_scales(uint32_t v) {
 template <int GB, int WM>
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
     const uint8_t* __restrict__ A6, const uint8_t* __restrict__ ea, const uint8_t* __restrict__ W6,
-    const uint8_t* __restrict__ ew, int M, int N, int K, uint16_t* __restrict__ Y) {
+    const uint8_t* __restrict__ ew, int M, int N, int K, uint16_t* __restrict__ Y, int nks_split,
+    float* __restrict__ part) {
     constexpr int BM = 128 * WM, BN = 256, MI = 4, NJ = WM, WN = 8 / WM;
     constexpr int ACH = (BM * 6 + 511) / 512;  // 16-byte activation chunks per thread and stage
     __shared__ StageMX<BM> st[2];
@@ -173,7 +174,9 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int wm = wave / WN, wn = wave % WN;
     const int l32 = lane & 31, lh = lane >> 5;
-    const int nks = K / 128;
+    // K range: stages [kofs, kofs + nks) of this workgroup's split (blockIdx.y)
+    const int nks = nks_split;
+    const int kofs = static_cast<int>(blockIdx.y) * nks_split;
     const uint32_t rowb = static_cast<uint32_t>(3 * K / 4);
     const int ng = K / (32 * GB);
 
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
     uint4 ra0, ra1, ra2, rw0, rw1, rw2;
     uint32_t rsc = 0;
     auto load = [&](int s) __attribute__((always_inline)) {
-        s = min(s, nks - 1);
+        s = min(s, nks - 1) + kofs;
         const uint8_t* abase = A6 + static_cast<int64_t>(s) * MX_SROW;
         ra0 = *reinterpret_cast<const uint4*>(abase + ag0);
         if (a1) ra1 = *reinterpret_cast<const uint4*>(abase + ag1);
@@ -290,7 +293,8 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
         __syncthreads();
     }
 
-    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3, of each block
+    // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3, of each
+    // block; a split writes its fp32 partial tile to part[split][m][n] instead
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         const int gm = m0 + wm * 128 + i * 32 + l32;
@@ -299,6 +303,19 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_mx_kernel(
         for (int j = 0; j < NJ; ++j) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
+                if (part) {
+                    const int gn = n0 + wn * 32 * NJ + j * 32 + 8 * q + 4 * lh;
+                    float* dst = part + static_cast<int64_t>(blockIdx.y) * M * N + static_cast<int64_t>(gm) * N + gn;
+                    if ((N & 3) == 0 && gn + 3 < N) {
+                        *reinterpret_cast<float4*>(dst) = make_float4(D[i][j][4 * q], D[i][j][4 * q + 1],
+                                                                      D[i][j][4 * q + 2], D[i][j][4 * q + 3]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (gn + e < N) dst[e] = D[i][j][4 * q + e];
+                    }
+                    continue;
+                }
                 const uint32_t h01 = __half_as_ushort(__float2half_rn(D[i][j][4 * q + 0])) |
                                      (static_cast<uint32_t>(__half_as_ushort(__float2half_rn(D[i][j][4 * q + 1]))) << 16);
                 const uint32_t h23 = __half_as_ushort(__float2half_rn(D[i][j][4 * q + 2])) |
@@ -328,22 +345,53 @@ hipError_t launch_quant_mx_b(const uint16_t* x, int64_t M, int64_t K, uint8_t* q
     return hipGetLastError();
 }
 
+// Split factor over K for the 128 x 256 tiling when it leaves CUs idle: the
+// largest S in {2, 4, 8} with tiles * S <= CUs, S dividing the stage count and
+// at least 4 stages per split; 1 where no split applies or the 256 x 256
+// tiling already fills the CUs.
+int mx_split_factor(int64_t M, int64_t N, int64_t K) {
+    const int64_t cus = device_cu_count();
+    if (((M + 255) / 256) * ((N + 255) / 256) >= cus) return 1;
+    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    const int64_t nks = K / 128;
+    int S = 1;
+    for (int c = 2; c <= 8; c *= 2)
+        if (tiles * c <= cus && nks % c == 0 && nks / c >= 4) S = c;
+    return S;
+}
+
 template <int GB>
 hipError_t launch_gemm_mx_g(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
-                            int64_t N, int64_t K, uint16_t* Y, hipStream_t stream) {
+                            int64_t N, int64_t K, uint16_t* Y, int S, float* part, hipStream_t stream) {
+    const int nks = static_cast<int>(K / 128);
     // 256-row tiles where they still give every CU a workgroup
     const int64_t big = ((M + 255) / 256) * ((N + 255) / 256);
-    if (big >= device_cu_count()) {
+    if (S == 1 && big >= device_cu_count()) {
         if (big > 0x7FFFFFFF) return hipErrorInvalidValue;
         hipLaunchKernelGGL((w4a4_gemm_mx_kernel<GB, 2>), dim3(static_cast<unsigned>(big)), dim3(512), 0, stream, A6, ea,
-                           W6, ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+                           W6, ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y, nks,
+                           static_cast<float*>(nullptr));
         return hipGetLastError();
     }
     const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((w4a4_gemm_mx_kernel<GB, 1>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, A6, ea,
-                       W6, ew, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y);
+    hipLaunchKernelGGL((w4a4_gemm_mx_kernel<GB, 1>), dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)),
+                       dim3(512), 0, stream, A6, ea, W6, ew, static_cast<int>(M), static_cast<int>(N),
+                       static_cast<int>(K), Y, nks / S, S > 1 ? part : static_cast<float*>(nullptr));
     return hipGetLastError();
+}
+
+hipError_t gemm_mx_dispatch(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
+                            int64_t N, int64_t K, int64_t G, uint16_t* Y, int S, float* part, hipStream_t stream) {
+    switch (G) {
+        case 32: return launch_gemm_mx_g<1>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        case 64: return launch_gemm_mx_g<2>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        case 128: return launch_gemm_mx_g<4>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        case 256: return launch_gemm_mx_g<8>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        case 512: return launch_gemm_mx_g<16>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        case 1024: return launch_gemm_mx_g<32>(A6, ea, W6, ew, M, N, K, Y, S, part, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
@@ -363,15 +411,23 @@ hipError_t launch_quant_mx(const uint16_t* x, int64_t M, int64_t K, int64_t G, u
 
 hipError_t launch_gemm_mx(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew, int64_t M,
                           int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
-    switch (G) {
-        case 32: return launch_gemm_mx_g<1>(A6, ea, W6, ew, M, N, K, Y, stream);
-        case 64: return launch_gemm_mx_g<2>(A6, ea, W6, ew, M, N, K, Y, stream);
-        case 128: return launch_gemm_mx_g<4>(A6, ea, W6, ew, M, N, K, Y, stream);
-        case 256: return launch_gemm_mx_g<8>(A6, ea, W6, ew, M, N, K, Y, stream);
-        case 512: return launch_gemm_mx_g<16>(A6, ea, W6, ew, M, N, K, Y, stream);
-        case 1024: return launch_gemm_mx_g<32>(A6, ea, W6, ew, M, N, K, Y, stream);
-        default: return hipErrorInvalidValue;
-    }
+    return gemm_mx_dispatch(A6, ea, W6, ew, M, N, K, G, Y, 1, nullptr, stream);
+}
+
+int64_t mx_splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G) {
+    (void)G;
+    const int S = M > 0 ? mx_split_factor(M, N, K) : 1;
+    return S > 1 ? static_cast<int64_t>(S) * M * N * static_cast<int64_t>(sizeof(float)) : 0;
+}
+
+hipError_t launch_gemm_mx_splitk(const uint8_t* A6, const uint8_t* ea, const uint8_t* W6, const uint8_t* ew,
+                                 int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
+                                 hipStream_t stream) {
+    const int S = mx_split_factor(M, N, K);
+    if (S < 2) return launch_gemm_mx(A6, ea, W6, ew, M, N, K, G, Y, stream);
+    const hipError_t e = gemm_mx_dispatch(A6, ea, W6, ew, M, N, K, G, Y, S, part, stream);
+    if (e != hipSuccess) return e;
+    return launch_splitk_reduce(part, S, M * N, Y, stream);
 }
 
 }  // namespace apex4

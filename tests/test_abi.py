@@ -37,8 +37,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
               "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
-              "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_status_string",
-              "apex4_version"):
+              "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
+              "apex4_w4a4_gemm_mx_ws", "apex4_status_string", "apex4_version"):
         assert f in names
 
 
@@ -199,6 +199,15 @@ def test_mx_validation(L):
     assert g(*ok, 4, 8, 256, 48, h.ptr(), s) == -3
     assert g(*ok, 1 << 20, 8, 6144, 128, h.ptr(), s) == -2          # A_6 of 4.5 GiB
     assert g(*ok, 4, 8, 256, 128, h.ptr(2), s) == -4
+    q = L.apex4_w4a4_gemm_mx_workspace_size
+    b = ctypes.c_int64(-1)
+    assert q(4, 8, 256, 128, None) == -1
+    assert q(4, 8, 200, 128, ctypes.byref(b)) == -2
+    assert q(4, 8, 256, 96, ctypes.byref(b)) == -3 and b.value == -1
+    w = L.apex4_w4a4_gemm_mx_ws
+    assert w(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), h.ptr(), 1 << 20, s) == -1
+    assert w(*ok, 4, 8, 256, 64 * 3, h.ptr(), h.ptr(), 1 << 20, s) == -3
+    assert w(*ok, 4, 8, 256, 128, h.ptr(), h.ptr(4), 1 << 20, s) == -4   # misaligned workspace
 
 
 def test_device_check_without_gpu():

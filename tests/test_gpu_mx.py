@@ -119,3 +119,44 @@ def test_group_rule_and_empty():
     assert m.apex4_w4a4_gemm_mx(A6, ea, W6, ew, 128).shape == (0, 8)
     with pytest.raises(m.Apex4Error):
         m.apex4_w4a4_gemm_mx(A6, ea, W6, ew, 256)                  # G > K
+
+
+# split over K (apex4_w4a4_gemm_mx_ws): factors 4, 4, 2 and an odd M N (the
+# reduction's one-element path)
+MX_SPLIT = [(256, 8192, 8192, 128), (64, 1024, 2048, 32), (512, 8192, 4096, 64), (65, 1001, 2048, 128)]
+
+
+@pytest.mark.parametrize("M,N,K,G", MX_SPLIT)
+def test_split_k(M, N, K, G):
+    import torch
+    m = pk()
+    need = m.apex4_w4a4_gemm_mx_workspace_size(M, N, K, G)
+    log(f"mx split-K M={M} N={N} K={K} G={G} workspace={need}")
+    assert need > 0 and need % (4 * M * N) == 0
+    r = np.random.default_rng(M + N + K + G)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    ea = (127 + r.integers(-6, 3, size=(M, K // G))).astype(np.uint8)
+    ew = (127 + r.integers(-6, 3, size=(N, K // G))).astype(np.uint8)
+    d = (dev(ofp6.pack_fp6(Aq)), dev(ea), dev(ofp6.pack_fp6(Wq)), dev(ew))
+    ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
+    Y1 = host(m.apex4_w4a4_gemm_mx_ws(*d, G, ws))
+    Y2 = host(m.apex4_w4a4_gemm_mx_ws(*d, G, ws))
+    assert np.array_equal(Y1.view(np.uint16), Y2.view(np.uint16))
+    rows = sample_rows(M, seed=M) if M > 64 else np.arange(M)
+    check_tolerance(Y1[rows], omx.gemm_mx_f64(Aq, ea, Wq, ew, K, G, rows), f"mx split {M}x{N}x{K} G{G}")
+    with pytest.raises(m.Apex4Error) as e:
+        m.apex4_w4a4_gemm_mx_ws(*d, G, ws[: need - 16])
+    assert e.value.status == -7
+
+
+def test_no_split_is_the_plain_mx_gemm():
+    m = pk()
+    M, N, K, G = 2048, 8192, 1024, 128
+    assert m.apex4_w4a4_gemm_mx_workspace_size(M, N, K, G) == 0
+    r = np.random.default_rng(9)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    ea = (127 + r.integers(-3, 3, size=(M, K // G))).astype(np.uint8)
+    ew = (127 + r.integers(-3, 3, size=(N, K // G))).astype(np.uint8)
+    d = (dev(ofp6.pack_fp6(Aq)), dev(ea), dev(ofp6.pack_fp6(Wq)), dev(ew))
+    assert np.array_equal(host(m.apex4_w4a4_gemm_mx(*d, G)).view(np.uint16),
+                          host(m.apex4_w4a4_gemm_mx_ws(*d, G)).view(np.uint16))
