@@ -240,6 +240,12 @@ LAYER_CONFIGS = {
             ("down", 8192, 28672, 32)],
 }
 LAYER_M = (16, 256, 4096)
+# The MX variant (power-of-two group scales inside the FP6 MFMA; not the
+# paper's fp16 scales) on the same linears, uniformly at G = 32 and G = 128.
+MX_LAYER_CONFIGS = {
+    "mx_g32": [(n, N_, K_, 32) for n, N_, K_, _ in LAYER_CONFIGS["g128"]],
+    "mx_g128": [(n, N_, K_, 128) for n, N_, K_, _ in LAYER_CONFIGS["g128"]],
+}
 
 
 def layers_mode(reps: int = 10):
@@ -332,6 +338,38 @@ def layers_mode(reps: int = 10):
                               "k_splits": split, "total_us": round(sum(per.values()), 2)}), flush=True)
         del wsets
         torch.cuda.empty_cache()
+    # the MX variant: quantize_mx, then the MX GEMM (split over K with a workspace where it applies)
+    for cfg, linears in MX_LAYER_CONFIGS.items():
+        wsets = {}
+        for name, Nl, Kl, Gl in linears:
+            W6 = pk.apex4_pack_fp6(torch.from_numpy(wl.random_codes(r, Nl, Kl)).to(dev))
+            ew = torch.from_numpy((127 + r.integers(-4, 2, size=(Nl, Kl // Gl))).astype(np.uint8)).to(dev)
+            R = copies(3 * Nl * Kl // 4 + Nl * (Kl // Gl))
+            wsets[name] = [(W6, ew)] + [(W6.clone(), ew.clone()) for _ in range(R - 1)]
+        for Ml in LAYER_M:
+            per, gbs, split = {}, {}, {}
+            for name, Nl, Kl, Gl in linears:
+                x = torch.from_numpy(wl.activations(wl.rng_for("llama70b", 98, Ml + Kl), Ml, Kl)).to(dev)
+                Y = torch.empty((Ml, Nl), dtype=torch.float16, device=dev)
+                A6 = torch.empty((Ml, 3 * Kl // 4), dtype=torch.uint8, device=dev)
+                ea = torch.empty((Ml, Kl // Gl), dtype=torch.uint8, device=dev)
+                ws = wsets[name]
+                need = pk.apex4_w4a4_gemm_mx_workspace_size(Ml, Nl, Kl, Gl)
+                work = torch.empty((max(need, 16),), dtype=torch.uint8, device=dev)
+
+                def call(i):
+                    pk.apex4_quantize_mx(x, Gl, A6, ea)
+                    pk.apex4_w4a4_gemm_mx_ws(A6, ea, ws[i % len(ws)][0], ws[i % len(ws)][1], Gl, work, Y)
+                t = graph_timed(call, reps)
+                per[name] = round(t, 2)
+                nbytes = 2 * Ml * Kl + 3 * Ml * Kl / 4 + 3 * Nl * Kl / 4 + (Ml + Nl) * Kl / Gl + 2 * Ml * Nl
+                gbs[name] = round(nbytes / (t * 1e-6) / 1e9)
+                split[name] = need // (4 * Ml * Nl) if need else 1
+                del x, Y, A6, ea, work
+            print(json.dumps({"mode": "layers", "config": cfg, "M": Ml, "linear_us": per, "hbm_gbs": gbs,
+                              "k_splits": split, "total_us": round(sum(per.values()), 2)}), flush=True)
+        del wsets
+        torch.cuda.empty_cache()
     # fp16 GEMMs of the same shapes (the value projection is part of qkv)
     shapes = [("qkv", 10240, 8192), ("o", 8192, 8192), ("gate_up", 57344, 8192), ("down", 8192, 28672)]
     for Ml in LAYER_M:
@@ -367,6 +405,17 @@ def summarize_layers(path, command):
             continue
         lines.append(f"| {Ml} | {g['total_us']} | {mx['total_us']} | {f['total_us']} | "
                      f"{f['total_us'] / g['total_us']:.2f} | {f['total_us'] / mx['total_us']:.2f} |")
+    if any(r["config"].startswith("mx_") for r in rows):
+        lines += ["", "MX variant (power-of-two group scales applied inside the FP6 MFMA, no per-group "
+                  "dequantization; not the paper's fp16 scales): apex4_quantize_mx + apex4_w4a4_gemm_mx_ws.", "",
+                  "| M | MX G=32 us | MX G=128 us | fp16 us | MX G=32 speedup vs fp16 | MX G=128 speedup vs fp16 |",
+                  "|---|---|---|---|---|---|"]
+        for Ml in sorted({r["M"] for r in rows}):
+            a, b, f = tot.get(("mx_g32", Ml)), tot.get(("mx_g128", Ml)), tot.get(("fp16", Ml))
+            if not (a and b and f):
+                continue
+            lines.append(f"| {Ml} | {a['total_us']} | {b['total_us']} | {f['total_us']} | "
+                         f"{f['total_us'] / a['total_us']:.2f} | {f['total_us'] / b['total_us']:.2f} |")
     lines += ["", "Per linear (us; W4A4 rows also give the algorithmic HBM GB/s of x, codes, scales and Y):", "",
               "| config | M | per linear |", "|---|---|---|"]
     for r in rows:
