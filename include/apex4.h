@@ -126,12 +126,13 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
 /*
  * Workspace form of apex4_w4a4_gemm for shapes that leave compute units idle
  * (Eq. (group_decomposition) split over K; the striped work decomposition of
- * Sec. 4.2 across workgroups).  When the 128 x 256 tiles of a G = 128 GEMM
- * number fewer than the compute units (M > 32), K is split into S in {2, 4, 8}
- * ranges of whole groups; each workgroup writes an fp32 partial tile into the
- * workspace, and a second kernel sums the S partials in range order and rounds
- * once to binary16.  Y is then within the tolerance of apex4_w4a4_gemm (the
- * fp32 summation order differs), deterministic for a given shape and device.
+ * Sec. 4.2 across workgroups).  When the GEMM's tiles number too few for the
+ * compute units (M > 32), K is split into S in {2, 4, 8} ranges of whole
+ * groups; each workgroup writes a partial tile into the workspace (fp32, or
+ * the exact int32 sums for G == K), and a second kernel sums the S partials in
+ * range order and rounds once to binary16.  Y is then within the tolerance of
+ * apex4_w4a4_gemm (the fp32 summation order differs; for G == K it is the same
+ * bits), deterministic for a given shape and device.
  *
  * apex4_w4a4_gemm_workspace_size writes to *bytes the workspace this shape
  * needs on the current device: S * M * N * 4, or 0 where no split applies (then

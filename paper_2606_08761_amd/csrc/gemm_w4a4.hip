@@ -52,6 +52,11 @@
 //     dequant phases half a stage apart (described at the kernel).  Small tiles
 //     (64 x 128) may split K over two wave groups (KSPLIT) and keep PF stages
 //     of loads in flight.
+//   * Split-K across workgroups (launch_gemm_splitk, G == 128, caller
+//     workspace): when the 128 x 256 tiles leave CUs idle, the ping-pong kernel
+//     runs on a tiles x S grid, each workgroup over S-th of the stages, and
+//     writes its fp32 partial tile; splitk_reduce_kernel adds the S partials
+//     in range order and rounds once.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -124,7 +129,7 @@ template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P) {
+    int32_t* __restrict__ P, int nks_split, void* __restrict__ part) {
     constexpr int NT = 64 * WAVES_M * WAVES_N;
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     constexpr int A_CH = BM * 4 / NT;                 // 16-byte packed activation chunks per thread
@@ -170,8 +175,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     const int wave = tid >> 6, lane = tid & 63;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int l32 = lane & 31, lh = lane >> 5;
-    const int nks = K / KS / KSPLIT;  // stages of this K-group
-    const int kbase = kg * nks;       // its first stage
+    // stages of this K-group, and its first stage: a workgroup covers
+    // nks_split stages from blockIdx.y * nks_split (split-K across workgroups)
+    const int nks = nks_split / KSPLIT;
+    const int kbase = static_cast<int>(blockIdx.y) * nks_split + kg * nks;
     const int spg = FINE ? 1 : G / KS;  // stages per group
     const int ng = K / G;
 
@@ -525,6 +532,37 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     // The last step stored a copy of the final stage (and its scales) into the
     // buffer it did not read, so either buffer holds the final scales.
     const int lastbuf = nks & 1;
+    if (part) {
+        // split-K: this workgroup's partial tile, fp32 (exact int32 sums for
+        // kChannel), to plane blockIdx.y of part[S][M][N]
+        int32_t* pbase = static_cast<int32_t*>(part) + static_cast<int64_t>(blockIdx.y) * M * N;
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+            const int gm = m0 + wm * MI * 32 + i * 32 + l32;
+            if (gm >= M) continue;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    int32_t v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if constexpr (MODE == kChannel) v[e] = psum[i][j][4 * q + e];
+                        else v[e] = __float_as_int(acc[i][j][4 * q + e]);
+                    }
+                    const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * q + 4 * lh;
+                    int32_t* dst = pbase + static_cast<int64_t>(gm) * N + gn;
+                    if ((N & 3) == 0 && gn + 3 < N) {
+                        *reinterpret_cast<int4*>(dst) = make_int4(v[0], v[1], v[2], v[3]);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (gn + e < N) dst[e] = v[e];
+                    }
+                }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
         const int gm = m0 + wm * MI * 32 + i * 32 + l32;
@@ -819,7 +857,8 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
 
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT>
 hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                    int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+                    int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
+                    void* part = nullptr) {
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
@@ -829,8 +868,9 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
     // the deeper ring costs occupancy and time, so those keep one stage.
     constexpr int PF = (WAVES_M * WAVES_N * MI * NJ <= 8 && GPS == 1) ? 4 : 1;
     hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT>),
-                       dim3(static_cast<unsigned>(tiles)), dim3(64 * WAVES_M * WAVES_N * KSPLIT), 0, stream, Aq, sa, Wq,
-                       sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), static_cast<int>(G), Y, P);
+                       dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(64 * WAVES_M * WAVES_N * KSPLIT),
+                       0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
+                       static_cast<int>(G), Y, P, static_cast<int>(K / KS / S), part);
     return hipGetLastError();
 }
 
@@ -842,8 +882,12 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
 // fit twice, and the split loses (N = 10240: 9 % slower).
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
 hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
+                  void* part = nullptr) {
     constexpr bool small = WAVES_M * WAVES_N * MI * NJ <= 8;
+    if (S > 1)  // split across workgroups: one wave group per workgroup
+        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S,
+                                                                          part);
     if constexpr (small && MODE != kDump) {
         constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
         const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
@@ -864,18 +908,20 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
 // (decode) to the streaming kernel instead, except for the debug dump.
 template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                        int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream) {
+                        int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
+                        void* part = nullptr) {
     if (P) {
         if (G == 32) return launch<1, WAVES_N, MI, 1, kDump, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         if (G == 64) return launch<1, WAVES_N, MI, 1, kDump, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         if (G <= 256) return launch<1, WAVES_N, MI, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
         return launch<1, WAVES_N, MI, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
     }
-    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
     if (G == 128) {
         if constexpr (WAVES_N == 8 && MI == 4) {
+            if (S > 1) return hipErrorInvalidValue;
             const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
             if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
             hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, Aq, sa, Wq,
@@ -883,10 +929,10 @@ hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq
                                static_cast<int>(K / KS), static_cast<float*>(nullptr));
             return hipGetLastError();
         }
-        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
     }
-    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
 }
 
 namespace {
@@ -922,29 +968,62 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
 }
 
+// Per-channel split-K: the S planes hold exact int32 sums of 256 P; their sum
+// is scaled exactly as the per-channel epilogue does, so Y is the same bits as
+// without the split.
+__global__ __launch_bounds__(256) void splitk_reduce_channel_kernel(const int32_t* __restrict__ part, int S, int M,
+                                                                    int N, const uint16_t* __restrict__ sa,
+                                                                    const uint16_t* __restrict__ sw,
+                                                                    uint16_t* __restrict__ Y) {
+    const int64_t MN = static_cast<int64_t>(M) * N;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < MN; i += stride) {
+        int32_t p = part[i];
+        for (int sp = 1; sp < S; ++sp) p += part[sp * MN + i];
+        const int64_t m = i / N, n = i - m * N;
+        const float sav = h2f(sa[m]) * (1.0f / 256.0f);
+        const float v = static_cast<float>(p) * sav * h2f(sw[n]);
+        Y[i] = __half_as_ushort(__float2half_rn(v));
+    }
+}
+
 }  // namespace
 
-// Split factor for the G = 128 tile kernel when it leaves CUs idle: the
-// largest S in {2, 4, 8} with tiles * S <= CUs, S dividing the stage count and
-// at least 4 stages per split; 1 where no split applies.  S = 2 is taken only
-// from M = 256 on: below that the 128-row tiles are half empty and the
-// 64 x 128 tiles of launch_gemm, which already fill the CUs, were faster
-// (MI355X, M = 64, N = 28672, K = 8192: 39.5 us against 49.6 us split).
+// Split factor over K when the tiles leave CUs idle; 1 where no split applies.
+//   * G = 128: the ping-pong kernel's 128 x 256 tiles, the largest S in
+//     {2, 4, 8} with tiles * S <= CUs, S dividing the stage count and at least
+//     4 stages per split.  S = 2 is taken only from M = 256 on: below that the
+//     128-row tiles are half empty and the 64 x 128 tiles of launch_gemm,
+//     which already fill the CUs, were faster (MI355X, M = 64, N = 28672,
+//     K = 8192: 39.5 us against 49.6 us split).
+//   * Other G: the 64 x 128 tiles of four waves (two workgroups per CU), when
+//     they fill at most half the CUs (above that the in-workgroup K split of
+//     launch already gives every SIMD two waves): the largest S with
+//     tiles * S <= 2 CUs, splits starting on group boundaries, at least 4
+//     stages each.
 int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G) {
-    if (G != 128 || M <= 0 || gemv_fits(M, N, K, G) || decode_fits(M, N, K, G)) return 1;
-    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    if (M <= 0 || gemv_fits(M, N, K, G) || decode_fits(M, N, K, G)) return 1;
     const int64_t cus = device_cu_count();
-    if (tiles >= cus) return 1;
     const int64_t nks = K / KS;
+    if (((M + 127) / 128) * ((N + 255) / 256) >= cus) return 1;
     int S = 1;
+    if (G == 128) {
+        const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+        for (int c = 2; c <= 8; c *= 2)
+            if (tiles * c <= cus && nks % c == 0 && nks / c >= 4) S = c;
+        return (S == 2 && M < 256) ? 1 : S;
+    }
+    const int64_t tiles = ((M + 63) / 64) * ((N + 127) / 128);
+    if (2 * tiles > cus) return 1;
+    const int64_t spg = (G == K || G <= KS) ? 1 : G / KS;
     for (int c = 2; c <= 8; c *= 2)
-        if (tiles * c <= cus && nks % c == 0 && nks / c >= 4) S = c;
-    return (S == 2 && M < 256) ? 1 : S;
+        if (tiles * c <= 2 * cus && nks % c == 0 && (nks / c) % spg == 0 && nks / c >= 4) S = c;
+    return S;
 }
 
 int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G) {
     const int S = splitk_factor(M, N, K, G);
-    return S > 1 ? static_cast<int64_t>(S) * M * N * static_cast<int64_t>(sizeof(float)) : 0;
+    return S > 1 ? static_cast<int64_t>(S) * M * N * 4 : 0;
 }
 
 hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* Y, hipStream_t stream) {
@@ -960,12 +1039,25 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
                               hipStream_t stream) {
     const int S = splitk_factor(M, N, K, G);
     if (S < 2) return launch_gemm(Aq, sa, Wq, sw, M, N, K, G, Y, nullptr, stream);
-    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
-    hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(512), 0,
-                       stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
-                       static_cast<int>(K / KS / S), part);
-    const hipError_t e = hipGetLastError();
+    hipError_t e;
+    if (G == 128) {
+        const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+        hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(512),
+                           0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
+                           static_cast<int>(K / KS / S), part);
+        e = hipGetLastError();
+    } else {
+        e = launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, nullptr, stream, S, part);
+    }
     if (e != hipSuccess) return e;
+    if (G == K) {
+        const int64_t need = (M * N + 255) / 256;
+        const int blocks = static_cast<int>(need < 8192 ? need : 8192);
+        hipLaunchKernelGGL(splitk_reduce_channel_kernel, dim3(blocks), dim3(256), 0, stream,
+                           reinterpret_cast<const int32_t*>(part), S, static_cast<int>(M), static_cast<int>(N), sa, sw,
+                           Y);
+        return hipGetLastError();
+    }
     return launch_splitk_reduce(part, S, M * N, Y, stream);
 }
 

@@ -1,5 +1,7 @@
 """GPU parity of the split-K GEMM (apex4_w4a4_gemm_ws; APEX4 Eq.
-group_decomposition summed over K ranges of whole groups, then over ranges).
+group_decomposition summed over K ranges of whole groups, then over ranges),
+for G = 128 (the ping-pong kernel) and the other group sizes (the general tile
+kernel; per-channel partials are exact, so that split is bit-identical).
 
   * where a split applies, Y is within |Y - y| <= 2e-3 |y| + 1e-2 RMS_row(y)
     of the oracle's binary64 y, and two calls give the same bits;
@@ -57,8 +59,8 @@ def test_split_matches_oracle(O, M, N, K):
                                       (64, 28672, 1024, 128)])
 def test_no_split_is_the_plain_gemm(M, N, K, GG):
     """No workspace needed: the same kernels as apex4_w4a4_gemm run (K = 384 has
-    too few stages per split, G != 128 has no split form, M = 64 with N = 28672
-    would only split in two)."""
+    too few stages per split; with G != 128 at M = 256, N = 8192 the small tiles
+    already fill the CUs; M = 64 with N = 28672 would only split in two)."""
     m = pk()
     assert m.apex4_w4a4_gemm_workspace_size(M, N, K, GG) == 0
     r = np.random.default_rng(M + N + K + GG)
@@ -81,3 +83,32 @@ def test_workspace_refused_when_short():
     with pytest.raises(m.Apex4Error) as e:
         m.apex4_w4a4_gemm_ws(*d, G, short)
     assert e.value.status == -7
+
+
+# the general tile kernel split over K: fine groups, persisting groups (splits
+# on group boundaries), per-channel (exact int32 partials)
+SPLIT_G = [(256, 1024, 8192, 32), (128, 2048, 4096, 64), (200, 1000, 4096, 256), (100, 1000, 2048, 1024),
+           (65, 1001, 2048, 32), (64, 2048, 8192, 8192), (300, 520, 3072, 3072)]
+
+
+@pytest.mark.parametrize("M,N,K,GG", SPLIT_G)
+def test_split_other_groups(O, M, N, K, GG):
+    import torch
+    m = pk()
+    need = m.apex4_w4a4_gemm_workspace_size(M, N, K, GG)
+    log(f"split-K M={M} N={N} K={K} G={GG} workspace={need}")
+    assert need > 0 and need // (4 * M * N) in (2, 4, 8)
+    r = np.random.default_rng(M * 7 + N + K + GG)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // GG), wl.random_scales(r, N, K // GG)
+    d = [dev(a) for a in (Aq, sa, Wq, sw)]
+    ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
+    Y1 = host(m.apex4_w4a4_gemm_ws(*d, GG, ws))
+    Y2 = host(m.apex4_w4a4_gemm_ws(*d, GG, ws))
+    assert np.array_equal(Y1.view(np.uint16), Y2.view(np.uint16))
+    if GG == K:
+        # per-channel partial sums are exact integers: the split changes no bit
+        Y0 = host(m.apex4_w4a4_gemm(*d, GG))
+        assert np.array_equal(Y1.view(np.uint16), Y0.view(np.uint16))
+    rows = sample_rows(M, seed=M) if M > 64 else np.arange(M)
+    check_tolerance(Y1[rows], O.gemm_rows(Aq, sa, Wq, sw, K, GG, rows), f"split-K {M}x{N}x{K} G{GG}")
