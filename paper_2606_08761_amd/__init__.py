@@ -280,18 +280,26 @@ class W4A4Linear:
         lin = W4A4Linear(weight_fp16_cuda, G=128)
         y = lin(x)             # x [..., K] float16 on the same device -> [..., N]
 
+    scales="mx" selects the MX variant instead: power-of-two group scales
+    applied inside the FP6 matrix instruction (apex4_quantize_mx +
+    apex4_w4a4_gemm_mx_ws; G in 32..1024) -- not the paper's fp16 scales.
+
     The work buffers for the quantized activations (and, for row counts whose
-    G = 128 GEMM is split over K, its workspace) are kept and reused while the
-    row count stays the same.  Bias and other dtypes are not supported: the
+    GEMM is split over K, its workspace) are kept and reused while the row
+    count stays the same.  Bias and other dtypes are not supported: the
     paper's layers are bias-free fp16 linears."""
 
-    def __init__(self, weight, G: int = 128):
+    def __init__(self, weight, G: int = 128, scales: str = "fp16"):
         import torch
         if weight.dim() != 2:
             raise ValueError("weight must be [N, K]")
+        if scales not in ("fp16", "mx"):
+            raise ValueError("scales must be 'fp16' or 'mx'")
         self.N, self.K = weight.shape
         self.G = self.K if G in (0, None) else int(G)
-        self.W_q, self.s_w = apex4_quantize_act(weight.contiguous(), self.G)
+        self.mx = scales == "mx"
+        quant = apex4_quantize_mx if self.mx else apex4_quantize_act
+        self.W_q, self.s_w = quant(weight.contiguous(), self.G)
         self._work = None
         self.device = weight.device
         self._torch = torch
@@ -304,12 +312,18 @@ class W4A4Linear:
         M = x2.shape[0]
         if self._work is None or self._work[0].shape[0] != M:
             torch = self._torch
-            need = apex4_w4a4_gemm_workspace_size(M, self.N, self.K, self.G) if M else 0
-            self._work = (torch.empty((M, self.K // 2), dtype=torch.uint8, device=x2.device),
-                          torch.empty((M, max(self.K // self.G, 1)), dtype=torch.float16, device=x2.device),
+            size = apex4_w4a4_gemm_mx_workspace_size if self.mx else apex4_w4a4_gemm_workspace_size
+            need = size(M, self.N, self.K, self.G) if M else 0
+            codes = (M, 3 * self.K // 4) if self.mx else (M, self.K // 2)
+            sdt = torch.uint8 if self.mx else torch.float16
+            self._work = (torch.empty(codes, dtype=torch.uint8, device=x2.device),
+                          torch.empty((M, max(self.K // self.G, 1)), dtype=sdt, device=x2.device),
                           torch.empty((need,), dtype=torch.uint8, device=x2.device) if need else None)
         Aq, sa, ws = self._work
-        if ws is None:
+        if self.mx:
+            apex4_quantize_mx(x2, self.G, Aq, sa)
+            Y = apex4_w4a4_gemm_mx_ws(Aq, sa, self.W_q, self.s_w, self.G, ws)
+        elif ws is None:
             Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, Aq, sa)
         else:
             apex4_quantize_act(x2, self.G, Aq, sa)

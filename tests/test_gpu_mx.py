@@ -160,3 +160,24 @@ def test_no_split_is_the_plain_mx_gemm():
     d = (dev(ofp6.pack_fp6(Aq)), dev(ea), dev(ofp6.pack_fp6(Wq)), dev(ew))
     assert np.array_equal(host(m.apex4_w4a4_gemm_mx(*d, G)).view(np.uint16),
                           host(m.apex4_w4a4_gemm_mx_ws(*d, G)).view(np.uint16))
+
+
+def test_linear_module_mx():
+    """W4A4Linear(scales="mx"): weights quantized once with power-of-two scales,
+    activations per call, against the oracle's MX quantize + GEMM (these row
+    counts take the split-K form with the layer's own workspace)."""
+    m = pk()
+    N, K, G = 1024, 2048, 64
+    x, w = wl.float_workload("tiny", 64, N, K)
+    lin = m.W4A4Linear(dev(w), G, scales="mx")
+    Wq_o, ew_o = omx.quantize_mx(w, G)
+    assert np.array_equal(host(lin.s_w), ew_o)
+    assert np.array_equal(host(lin.W_q), ofp6.pack_fp6(Wq_o))
+    for rows in (5, 64, 64):
+        y = host(lin(dev(x[:rows]).reshape(1, rows, K)))
+        assert y.shape == (1, rows, N)
+        assert (lin._work[2] is not None) == (m.apex4_w4a4_gemm_mx_workspace_size(rows, N, K, G) > 0)
+        Aq_o, ea_o = omx.quantize_mx(x[:rows], G)
+        check_tolerance(y[0], omx.gemm_mx_f64(Aq_o, ea_o, Wq_o, ew_o, K, G), f"mx module rows={rows}")
+    with pytest.raises(ValueError):
+        m.W4A4Linear(dev(w), G, scales="int8")
