@@ -18,12 +18,16 @@
 //     group (consecutive, aligned, in one wave) combine their maxima with
 //     cross-lane shuffles.  Codes are written as FP6 e3m2 (code k of a row at
 //     bits [6k, 6k + 6), 3K/4 bytes per row), scales as E8M0 bytes [rows, K/G].
-//   * w4a4_gemm_mx_kernel: 128 x 256 tiles, 8 waves of 128 x 32, both operands
-//     staged through LDS (16-byte chunks, six lanes per row-stage), one barrier
-//     per 128-wide stage.  Lane half h of MFMA kk holds the stage's codes
-//     [64h + 32kk, + 32) of its row, on both operands (as the FP6 kernel), so a
-//     lane's block lies in one group and its scale byte is block 2h + kk of the
-//     stage's four block scales (selected with the MFMA's op_sel).
+//   * w4a4_gemm_mx_kernel: 256 x 256 tiles of 2 x 4 waves of 128 x 64 where
+//     they fill the CUs, else 128 x 256 tiles of 8 waves of 128 x 32; both
+//     operands staged through LDS (16-byte chunks, six lanes per row-stage),
+//     one barrier per 128-wide stage.  Lane half h of MFMA kk holds the
+//     stage's codes [64h + 32kk, + 32) of its row, on both operands (as the
+//     FP6 kernel), so a lane's block lies in one group and its scale byte is
+//     block 2h + kk of the stage's four block scales (selected with the MFMA's
+//     op_sel).  Shapes that leave CUs idle may split K across workgroups into
+//     fp32 partial tiles (launch_gemm_mx_splitk, caller workspace), summed by
+//     the split-K reduction of the INT8 path.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
