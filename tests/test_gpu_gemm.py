@@ -6,7 +6,8 @@
     oracle's binary64 y;
   * workloads: tiny (M=64, N=K=1024) in full, the paper shape (M=2048,
     N=K=8192, G=128) on sampled rows, the Llama-2-70B linears, the granularity
-    sweep and the decode path, plus ragged and degenerate shapes.
+    sweep and the decode path, plus ragged and degenerate shapes, and operands
+    of the largest size the ABI accepts (just under 4 GiB).
 
 For the float workloads both sides quantize the same binary16 inputs
 independently (oracle quantizer on the host, HIP quantizer on the device).
@@ -341,3 +342,48 @@ def test_w4a4_linear_module(O):
     Aq_c, sa_c = O.quantize(x[:24], K)
     check_tolerance(host(lin_c(dev(x[:24]))), O.gemm_rows(Aq_c, sa_c, Wq_c, sw_c, K, K), "module per-channel")
     torch.cuda.synchronize()
+
+
+def test_weights_just_under_4gib(O):
+    """The largest weight operand the ABI accepts: N K/2 = 4,294,950,912 bytes,
+    16 KiB under 2^32 (the kernels address operand rows with 32-bit byte
+    offsets).  One row (dot-product kernel), 8 rows (decode kernel) and 40
+    rows (tile kernel), checked on sampled output columns that include the
+    last rows of W."""
+    import torch
+    m = pk()
+    N, K, G = 262143, 32768, 128
+    assert N * (K // 2) < 2 ** 32 and (N + 1) * (K // 2) >= 2 ** 32
+    log("4 GiB weights: generate")
+    r = np.random.default_rng(4096)
+    Wq = wl.random_codes(r, N, K)
+    sw = wl.random_scales(r, N, K // G)
+    Wq_d, sw_d = dev(Wq), dev(sw)
+    cols = np.unique(np.concatenate([np.arange(8), np.arange(N - 8, N), r.integers(0, N, size=24)]))
+    Wq_s, sw_s = Wq[cols], sw[cols]
+    del Wq
+    for M in (1, 8, 40):
+        log(f"4 GiB weights: M={M}")
+        Aq, sa = wl.random_codes(r, M, K), wl.random_scales(r, M, K // G)
+        Y = host(m.apex4_w4a4_gemm(dev(Aq), dev(sa), Wq_d, sw_d, G))
+        assert Y.shape == (M, N)
+        check_tolerance(Y[:, cols], O.gemm_rows(Aq, sa, Wq_s, sw_s, K, G), f"4 GiB weights M={M}")
+    del Wq_d, sw_d
+    torch.cuda.empty_cache()
+
+
+def test_activations_just_under_4gib(O):
+    """The largest activation operand: M K/2 = 4,294,950,912 bytes (tile kernel,
+    32-bit row offsets), checked on sampled rows that include the last ones."""
+    import torch
+    m = pk()
+    M, N, K, G = 262143, 40, 32768, 128
+    log("4 GiB activations: generate")
+    r = np.random.default_rng(4097)
+    Aq = wl.random_codes(r, M, K)
+    sa = wl.random_scales(r, M, K // G)
+    Wq, sw = wl.random_codes(r, N, K), wl.random_scales(r, N, K // G)
+    Y = host(m.apex4_w4a4_gemm(dev(Aq), dev(sa), dev(Wq), dev(sw), G))
+    rows = np.unique(np.concatenate([np.arange(4), np.arange(M - 130, M), r.integers(0, M, size=16)]))
+    check_tolerance(Y[rows], O.gemm_rows(Aq, sa, Wq, sw, K, G, rows), "4 GiB activations")
+    torch.cuda.empty_cache()
