@@ -47,7 +47,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers"), default="bench",
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers", "variants"),
+                   default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
                         "summarize: turn rocprofv3 CSV output into the profiles/ summaries")
@@ -62,6 +63,8 @@ def parse():
     p.add_argument("--gsweep-pmc", help="summarize: counter_collection.csv of the SQ counter pass over --mode gsweep")
     p.add_argument("--sq-csv", nargs="*", help="summarize: counter_collection.csv files of SQ counter passes over --mode counters")
     p.add_argument("--sq-commands", help="summarize: text file with the commands that made --sq-csv")
+    p.add_argument("--variants-sq-csv", nargs="*", help="summarize: counter_collection.csv files of SQ passes over --mode variants")
+    p.add_argument("--variants-commands", help="summarize: text file with the commands that made --variants-sq-csv")
     p.add_argument("--power-log", help="summarize: output of --mode power (written to profiles/power_clock_paper_shape.md)")
     p.add_argument("--power-command", default="python3 bench.py --mode power", help="summarize: the command that made --power-log")
     p.add_argument("--layers-log", help="summarize: output of --mode layers (written to profiles/layer_sweep_llama2_70b.md)")
@@ -147,6 +150,9 @@ def summarize_mode(args):
             summarize_layers(args.layers_log, args.layers_command)
         if args.sq_csv:
             summarize_sq(args.sq_csv, open(args.sq_commands).read().strip() if args.sq_commands else "")
+        if args.variants_sq_csv:
+            summarize_sq_variants(args.variants_sq_csv,
+                                  open(args.variants_commands).read().strip() if args.variants_commands else "")
         if args.power_log:
             summarize_power(args.power_log, args.power_command)
         if args.rho_json:
@@ -427,21 +433,22 @@ def summarize_layers(path, command):
         f.write("\n".join(lines) + "\n")
 
 
-def summarize_sq(paths, cmds):
-    """profiles/gemm_w4a4_sq_paper_shape.md: where the SIMD cycles of the
-    paper-shape G=128 GEMM go, from SQ counters (means over the GEMM dispatches
-    of bench.py --mode counters).  Quad-cycle counters are multiplied by 4;
-    per-SIMD figures divide by the 1024 SIMDs; the kernel's cycle count is
-    GRBM_GUI_ACTIVE over the 8 XCDs."""
+def _sq_means(paths, pick):
+    """Mean per dispatch of every counter over the CSV rows whose kernel pick() accepts."""
     import csv
     import statistics
     vals = {}
     for p in paths:
         for r in csv.DictReader(open(p)):
-            if not is_tiled_gemm(r["Kernel_Name"]):
-                continue
-            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-    c = {k: statistics.mean(v) for k, v in vals.items()}
+            if pick(r["Kernel_Name"]):
+                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return {k: statistics.mean(v) for k, v in vals.items()}
+
+
+def _sq_section(c, what, mfma):
+    """Where the SIMD cycles of one kernel go.  Quad-cycle counters are
+    multiplied by 4; per-SIMD figures divide by the 1024 SIMDs; the kernel's
+    cycle count is GRBM_GUI_ACTIVE over the 8 XCDs."""
     simds = 1024
     kcyc = c["GRBM_GUI_ACTIVE"] / 8
     quad = ["SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_VALU2",
@@ -449,13 +456,10 @@ def summarize_sq(paths, cmds):
             "SQ_WAIT_INST_LDS"]
     plain = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT"]
     mf = c["SQ_INSTS_MFMA"] / simds
-    lines = [f"# W4A4 GEMM, M={M} N=K={N} G={G}: SQ counters (where the SIMD cycles go)", "",
-             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
-             f"Kernel length: GRBM_GUI_ACTIVE / 8 XCDs = {kcyc:.0f} cycles. Per SIMD: {mf:.0f} MFMA "
-             f"(v_mfma_i32_32x32x32_i8), {c['SQ_INSTS_VALU'] / simds:.0f} VALU "
+    lines = [f"Kernel length ({what}): GRBM_GUI_ACTIVE / 8 XCDs = {kcyc:.0f} cycles. Per SIMD: {mf:.0f} MFMA "
+             f"({mfma}), {c['SQ_INSTS_VALU'] / simds:.0f} VALU "
              f"({c['SQ_INSTS_VALU'] / c['SQ_INSTS_MFMA']:.2f} per MFMA), {c['SQ_INSTS_LDS'] / simds:.0f} LDS, "
-             f"{c.get('SQ_INSTS_SALU', 0) / simds:.0f} SALU instructions; {kcyc / mf:.1f} cycles per MFMA per SIMD "
-             f"(32 at the MFMA peak).", "",
+             f"{c.get('SQ_INSTS_SALU', 0) / simds:.0f} SALU instructions; {kcyc / mf:.1f} cycles per MFMA per SIMD.", "",
              "| counter | per SIMD (cycles) | share of kernel cycles |", "|---|---|---|"]
     for k in quad:
         if k in c:
@@ -472,7 +476,34 @@ def summarize_sq(paths, cmds):
               f"* VALU cycles per VALU instruction: {c['SQ_ACTIVE_INST_VALU'] * 4 / c['SQ_INSTS_VALU']:.2f}",
               "", "Raw means per dispatch:", "", "| counter | value |", "|---|---|"]
     lines += [f"| {k} | {c[k]:.4g} |" for k in sorted(c)]
+    return lines
+
+
+def summarize_sq(paths, cmds):
+    """profiles/gemm_w4a4_sq_paper_shape.md: where the SIMD cycles of the
+    paper-shape G=128 GEMM go, from SQ counters (means over the GEMM dispatches
+    of bench.py --mode counters)."""
+    c = _sq_means(paths, is_tiled_gemm)
+    lines = [f"# W4A4 GEMM, M={M} N=K={N} G={G}: SQ counters (where the SIMD cycles go)", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", ""]
+    lines += _sq_section(c, "the G=128 GEMM", "v_mfma_i32_32x32x32_i8, 32 cycles at the MFMA peak")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_sq_paper_shape.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def summarize_sq_variants(paths, cmds):
+    """profiles/gemm_variants_sq_paper_shape.md: the same SQ breakdown for the
+    FP6-container and MX GEMMs (bench.py --mode variants)."""
+    lines = [f"# FP6 and MX variant GEMMs, M={M} N=K={N} G={G}: SQ counters", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", ""]
+    for title, key, mfma in (("FP6 containers, fp16 scales (w4a4_gemm_fp6_kernel)", "gemm_fp6_kernel",
+                              "v_mfma_scale_f32_32x32x64_f8f6f4, FP6 operands, unit scales"),
+                             ("MX, power-of-two scales (w4a4_gemm_mx_kernel<4, 2>)", "gemm_mx_kernel",
+                              "v_mfma_scale_f32_32x32x64_f8f6f4, FP6 operands, per-lane E8M0 scales")):
+        c = _sq_means(paths, lambda n, key=key: key in n)
+        if "GRBM_GUI_ACTIVE" in c and "SQ_INSTS_MFMA" in c:
+            lines += [f"## {title}", ""] + _sq_section(c, title.split(" (")[0], mfma) + [""]
+    with open(os.path.join(ROOT, "profiles", "gemm_variants_sq_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
 
@@ -662,6 +693,27 @@ def counters_mode():
                       "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
 
 
+def variants_mode():
+    """Launch the FP6-container and the MX GEMM (M=2048, N=K=8192, G=128) 3 times
+    each, nothing else, for per-dispatch counters."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    Aq, sa, Wq, sw = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("paper", M, N, K, G)]
+    A6, W6 = pk.apex4_pack_fp6(Aq), pk.apex4_pack_fp6(Wq)
+    ea = torch.full((M, K // G), 127, dtype=torch.uint8, device=dev)
+    ew = torch.full((N, K // G), 127, dtype=torch.uint8, device=dev)
+    Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        pk.apex4_w4a4_gemm_fp6(A6, sa, W6, sw, G, Y)
+    for _ in range(3):
+        pk.apex4_w4a4_gemm_mx(A6, ea, W6, ew, G, Y)
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "variants", "gemm": [M, N, K, G]}))
+
+
 GSWEEP = (4096, 8192, 8192, (32, 64, 128, 256, 512, 1024, 8192))
 GSWEEP_LAUNCHES = 23   # per group size: 3 warm-up + 20 timed
 
@@ -812,6 +864,8 @@ def main():
         return power_mode()
     if args.mode == "layers":
         return layers_mode()
+    if args.mode == "variants":
+        return variants_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
