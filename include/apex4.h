@@ -28,12 +28,15 @@
  * (M-sized when M == 0, the group-sum dump when mr == 0) may be NULL.  A failed launch returns
  * APEX4_ERR_LAUNCH.  Nothing is written when validation fails.
  *
- * Shape rules:  M >= 0, N >= 1, K >= 128 and K % 128 == 0, K % G == 0; each
- * packed operand of the GEMM entry points under 4 GiB (M K/2 and N K/2 below
- * 2^32 bytes).
+ * Shape rules (4-bit code entry points):  M >= 0, N >= 1, K >= 32 and
+ * K % 32 == 0, K % G == 0; each packed operand of the GEMM entry points under
+ * 4 GiB (M K/2 and N K/2 below 2^32 bytes).  The FP6 and MX entry points keep
+ * K >= 128 and K % 128 == 0.
  * Group sizes: the GEMM takes G in {32, 64, 128, 256, 512, 1024} or G == K
- * (per-channel); these are the granularities of Sec. 3.2.2 and Sec. 4.1.  The
- * quantizer takes any G with G % 32 == 0 and K % G == 0.
+ * (per-channel, K <= 65536: the kernels keep 256 times the row's integer sum,
+ * up to 2^14 K in magnitude, in one int32); these are the granularities of
+ * Sec. 3.2.2 and Sec. 4.1.  The quantizer takes any G with G % 32 == 0 and
+ * K % G == 0.
  * Alignment: every pointer 16-byte aligned.
  * Device: the current device must be gfx950 (MI355X / MI350X).
  */
@@ -95,15 +98,62 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a,
 
 /*
  * Debug form of apex4_w4a4_gemm: the exact integer group sums of Eq.
- * (group_decomposition), produced by the same GEMM kernel with a dump epilogue
- * in place of the dequantization.
+ * (group_decomposition).  The whole M x N problem runs through the kernel
+ * that apex4_w4a4_gemm picks for this shape (one-row, few-row or tile kernel),
+ * in its dump form with the scales and Y left out; only the window's sums are
+ * written.
  *
  *   P [mr, N, K/G] int32 (device, output): P[i, n, g] for rows m0 + i,
- *   0 <= m0, 0 <= mr, m0 + mr <= M.
+ *   0 <= m0, 0 <= mr, m0 + mr <= M; may be NULL when mr == 0.
  */
 int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
                               int64_t M, int64_t N, int64_t K, int64_t G,
                               int64_t m0, int64_t mr, int32_t* P, void* stream);
+
+/* flags of apex4_w4a4_gemm_debug */
+#define APEX4_DEBUG_GENERAL_TILES 1 /* tile kernel only: no one-row, few-row or G = 128 ping-pong kernel */
+
+/*
+ * Debug form of apex4_w4a4_gemm / apex4_w4a4_gemm_ws that returns, from the
+ * same launches that compute Y, the exact int32 group sums of Eq.
+ * (group_decomposition) for rows [m0, m0 + mr).
+ *
+ *   Operands and Y as apex4_w4a4_gemm.  workspace == NULL: the kernel choice
+ *   of apex4_w4a4_gemm; otherwise that of apex4_w4a4_gemm_ws (workspace as
+ *   there, including APEX4_ERR_WORKSPACE).
+ *   P [mr, N, K/G] int32 (device, output), window as in
+ *   apex4_w4a4_gemm_groupsums; mr == 0 writes no sums (P may be NULL).
+ *   flags: 0, or APEX4_DEBUG_GENERAL_TILES (other bits: APEX4_ERR_SHAPE).
+ * With flags == 0, Y is bit for bit the Y of the production entry point named
+ * above.  For tests and diagnostics; slower than the production calls.
+ */
+int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
+                          const uint8_t* W_q, const void* s_w,
+                          int64_t M, int64_t N, int64_t K, int64_t G,
+                          void* Y, void* workspace, int64_t workspace_bytes,
+                          int64_t m0, int64_t mr, int32_t* P, int flags, void* stream);
+
+/* entry points and kernels of apex4_w4a4_gemm_plan */
+#define APEX4_ENTRY_GEMM 0    /* apex4_w4a4_gemm (and _debug without workspace) */
+#define APEX4_ENTRY_GEMM_WS 1 /* apex4_w4a4_gemm_ws (and _debug with workspace) */
+#define APEX4_ENTRY_LINEAR 2  /* apex4_w4a4_linear (and _debug); its GEMM, after the quantizer */
+#define APEX4_KERNEL_GEMV 1       /* one row: v_dot8 on the packed codes */
+#define APEX4_KERNEL_FUSED 2      /* one row: quantizer fused into the GEMV's prologue */
+#define APEX4_KERNEL_DECODE 3     /* up to 32 rows: weights streamed once through the MFMA */
+#define APEX4_KERNEL_TILE_64 4    /* 64 x 128 output tiles */
+#define APEX4_KERNEL_TILE_128 5   /* 128 x 256 output tiles */
+#define APEX4_KERNEL_PINGPONG 6   /* G = 128 on 128 x 256 tiles, MFMA and dequant waves alternating */
+
+/*
+ * The GEMM kernel that `entry` runs for this shape on the current device, and
+ * its split over K (*splits = S > 1 only for APEX4_ENTRY_GEMM_WS, whose
+ * workspace size query then returns S M N 4 bytes).  flags as in
+ * apex4_w4a4_gemm_debug (0 for APEX4_ENTRY_LINEAR).  M == 0 gives kernel 0,
+ * splits 0.  Shape and group rules as apex4_w4a4_gemm; unknown entry or flags:
+ * APEX4_ERR_SHAPE.  Launches nothing.
+ */
+int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, int flags,
+                         int* kernel, int* splits);
 
 /*
  * Quantize-then-GEMM linear layer: the inference forward of one quantized
@@ -122,6 +172,16 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
 int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
                       int64_t M, int64_t N, int64_t K, int64_t G,
                       void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
+
+/*
+ * Debug form of apex4_w4a4_linear: the same kernels (fused or quantize + GEMM),
+ * Y and work buffers bit for bit, plus the exact int32 group sums of rows
+ * [m0, m0 + mr) into P [mr, N, K/G] as in apex4_w4a4_gemm_debug.
+ */
+int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w,
+                            int64_t M, int64_t N, int64_t K, int64_t G,
+                            void* Y, uint8_t* A_q_work, void* s_a_work,
+                            int64_t m0, int64_t mr, int32_t* P, void* stream);
 
 /*
  * Workspace form of apex4_w4a4_gemm for shapes that leave compute units idle

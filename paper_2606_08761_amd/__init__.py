@@ -22,10 +22,13 @@ LIB_PATH = os.path.join(HERE, "libapex4.so")
 
 APEX4_OK = 0
 STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
-          -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE"}
+          -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE", -7: "APEX4_ERR_WORKSPACE"}
+APEX4_DEBUG_GENERAL_TILES = 1
+ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2}
+KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong"}
 
-EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-            "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
+EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
+            "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
             "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
             "apex4_w4a4_gemm_mx_ws", "apex4_status_string", "apex4_version")
 
@@ -51,7 +54,10 @@ def lib() -> ctypes.CDLL:
     L.apex4_quantize_act.argtypes = [P, I, I, I, P, P, P]
     L.apex4_w4a4_gemm.argtypes = [P, P, P, P, I, I, I, I, P, P]
     L.apex4_w4a4_gemm_groupsums.argtypes = [P, P, I, I, I, I, I, I, P, P]
+    L.apex4_w4a4_gemm_debug.argtypes = [P, P, P, P, I, I, I, I, P, P, I, I, I, P, ctypes.c_int, P]
+    L.apex4_w4a4_gemm_plan.argtypes = [ctypes.c_int, I, I, I, I, ctypes.c_int, P, P]
     L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
+    L.apex4_w4a4_linear_debug.argtypes = [P, P, P, I, I, I, I, P, P, P, I, I, P, P]
     L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
     L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
     L.apex4_quantize_mx.argtypes = [P, I, I, I, P, P, P]
@@ -60,7 +66,8 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm_mx_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
-    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_linear",
+    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
+              "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug",
               "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
               "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
               "apex4_w4a4_gemm_mx_ws"):
@@ -169,6 +176,36 @@ def apex4_w4a4_gemm_groupsums(A_q, W_q, G: int, m0: int = 0, mr: int | None = No
     return P
 
 
+def _window(M, N, K, G, m0, mr, P, device):
+    import torch
+    if mr is None:
+        mr = M - m0
+    if P is None:
+        P = torch.empty((mr, N, max(K // G, 1)), dtype=torch.int32, device=device)
+    return mr, P
+
+
+def apex4_w4a4_gemm_debug(A_q, s_a, W_q, s_w, G: int, m0: int = 0, mr: int | None = None, workspace=None,
+                          flags: int = 0, Y=None, P=None, stream=None):
+    """Y of apex4_w4a4_gemm (workspace None) or apex4_w4a4_gemm_ws (workspace a
+    uint8 device tensor) and, from the same launches, the exact int32 group
+    sums P[i, n, g] of rows m0 .. m0+mr-1.  Returns (Y, P)."""
+    import torch
+    M, K2 = A_q.shape
+    N, K = W_q.shape[0], 2 * K2
+    mr, P = _window(M, N, K, G, m0, mr, P, A_q.device)
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
+    ws = ctypes.c_void_p(0) if workspace is None else _dev(workspace, torch.uint8, "workspace")
+    rc = lib().apex4_w4a4_gemm_debug(_dev(A_q, torch.uint8, "A_q"), _dev(s_a, torch.float16, "s_a"),
+                                     _dev(W_q, torch.uint8, "W_q"), _dev(s_w, torch.float16, "s_w"),
+                                     M, N, K, G, _dev(Y, torch.float16, "Y"), ws,
+                                     0 if workspace is None else workspace.numel(), m0, mr,
+                                     _dev(P, torch.int32, "P"), flags, _stream(A_q, stream))
+    _check("apex4_w4a4_gemm_debug", rc)
+    return Y, P
+
+
 def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None, stream=None):
     """Quantize x (SymQuant) then the W4A4 GEMM, both enqueued on one stream."""
     import torch
@@ -186,6 +223,37 @@ def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None,
                                  _dev(s_a_work, torch.float16, "s_a_work"), _stream(x, stream))
     _check("apex4_w4a4_linear", rc)
     return Y
+
+
+def apex4_w4a4_gemm_plan(entry: str, M: int, N: int, K: int, G: int, flags: int = 0):
+    """(kernel name, splits) that the entry point ("gemm", "gemm_ws" or
+    "linear") runs for this shape on the current device."""
+    k, s = ctypes.c_int(0), ctypes.c_int(0)
+    _check("apex4_w4a4_gemm_plan", lib().apex4_w4a4_gemm_plan(ENTRY[entry], M, N, K, G, flags, ctypes.byref(k),
+                                                              ctypes.byref(s)))
+    return KERNELS[k.value], int(s.value)
+
+
+def apex4_w4a4_linear_debug(x, W_q, s_w, G: int, m0: int = 0, mr: int | None = None, Y=None, A_q_work=None,
+                            s_a_work=None, P=None, stream=None):
+    """apex4_w4a4_linear plus the exact int32 group sums of rows m0 .. m0+mr-1
+    from the same kernels.  Returns (Y, A_q_work, s_a_work, P)."""
+    import torch
+    M, K = x.shape
+    N = W_q.shape[0]
+    mr, P = _window(M, N, K, G, m0, mr, P, x.device)
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    if A_q_work is None:
+        A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if s_a_work is None:
+        s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
+    rc = lib().apex4_w4a4_linear_debug(_dev(x, torch.float16, "x"), _dev(W_q, torch.uint8, "W_q"),
+                                       _dev(s_w, torch.float16, "s_w"), M, N, K, G, _dev(Y, torch.float16, "Y"),
+                                       _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
+                                       m0, mr, _dev(P, torch.int32, "P"), _stream(x, stream))
+    _check("apex4_w4a4_linear_debug", rc)
+    return Y, A_q_work, s_a_work, P
 
 
 def apex4_pack_fp6(q4, q6=None, stream=None):

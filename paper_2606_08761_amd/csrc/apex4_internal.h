@@ -7,26 +7,62 @@
 
 namespace apex4 {
 
+// Debug dump of the exact integer group sums P[m, n, g] (Eq. group_decomposition)
+// from the kernel that computes Y: rows [m0, m0 + mr) of the GEMM into
+// P[mr][N][K/G] (int32).  P == nullptr: no dump.  Kernels that add partial sums
+// of a group (K split over waves, 32-code dot products) add them with integer
+// atomics into a zeroed P; the others store each group sum once.
+struct Dump {
+    int32_t* P = nullptr;
+    int m0 = 0;
+    int mr = 0;
+};
+
+// K stages of 128 codes covering K (the last one partial when K % 128 != 0).
+inline int64_t kstages(int64_t K) { return (K + 127) / 128; }
+
 // Activation/weight quantizer (SymQuant, b = 4).
 hipError_t launch_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t G,
                            uint8_t* q, uint16_t* s, hipStream_t stream);
 
-// W4A4 GEMM.  When P is non-null the kernel dumps the exact integer group sums
-// of rows [0, M) of the given operands instead of dequantizing (Y unused).
+// Kernel choice of the W4A4 GEMM entry points (values of the public
+// APEX4_KERNEL_* constants).
+enum GemmKernel : int {
+    kKernelGemv = 1,      // one row, v_dot8 on the packed codes
+    kKernelFused = 2,     // one row, quantize in the prologue (linear only)
+    kKernelDecode = 3,    // up to 32 rows, weights streamed once
+    kKernelTile64 = 4,    // 64 x 128 tiles, 4 waves (K may split inside the workgroup)
+    kKernelTile128 = 5,   // 128 x 256 tiles, 8 waves
+    kKernelPingPong = 6,  // G = 128 on 128 x 256 tiles, ping-pong schedule
+};
+struct GemmPlan {
+    GemmKernel kernel;
+    int splits;  // S > 1: split over K across workgroups (workspace path)
+};
+// split: the workspace path may split K; force_tile: no one-row, few-row or
+// ping-pong kernel (tests compare the general tile kernel against them).
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile);
+
+// W4A4 GEMM: the one-row, few-row or tile kernel by shape (force_tile: always
+// the tile kernel, for tests).  With a dump, the same kernel also writes the
+// window's group sums; sa == sw == nullptr then skips the scales and Y.
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                        const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
-                       uint16_t* Y, int32_t* P, hipStream_t stream);
+                       uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool force_tile = false);
 
-// G = 128 GEMM split over K across workgroups for shapes whose 128 x 256 tiles
-// leave CUs idle: S fp32 partial planes part[S][M][N] (caller workspace of
-// splitk_workspace_bytes bytes), summed in split order and rounded once.
+// int32 fill of n elements (dump buffers that receive atomic partial sums).
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream);
+
+// GEMM split over K across workgroups for shapes whose tiles leave CUs idle:
+// S partial planes part[S][M][N] (fp32, or int32 for G = K; caller workspace
+// of splitk_workspace_bytes bytes), summed in split order and rounded once.
 // splitk_factor() == 1 (workspace 0) where no split applies; launch_gemm_splitk
-// then runs launch_gemm.
+// then runs launch_gemm.  force_tile: G = 128 on the general tile kernel.
 int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G);
 int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
-                              hipStream_t stream);
+                              hipStream_t stream, Dump dump = Dump(), bool force_tile = false);
 
 // Y = binary16(sum of the S fp32 planes part[S][M N]) in plane order.
 hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* Y, hipStream_t stream);
@@ -39,14 +75,14 @@ int device_cu_count();
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                               const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
-                              uint16_t* Y, hipStream_t stream);
+                              uint16_t* Y, hipStream_t stream, Dump dump = Dump());
 
 // W4A4 GEMM for one row on the vector ALUs (v_dot8_i32_i4 on the packed
 // codes): weight rows streamed from HBM in 1 KB runs.  gemv_fits() says
 // whether the shape is one it handles.
 bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream);
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump = Dump());
 
 // Quantize + W4A4 GEMM in one kernel: the one-row kernel above, quantizing x
 // in its prologue (G in {32, 64, 128, 256, 512}, G < K).  Y as
@@ -54,7 +90,8 @@ hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
 // receive the same codes and scales as launch_quantize writes.
 bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N,
-                               int64_t K, int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream);
+                               int64_t K, int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream,
+                               Dump dump = Dump());
 
 // The 4-bit codes in FP6 e3m2 containers (6-bit fields, little-endian, 3K/4
 // bytes per row) and the G = 128 GEMM on the FP6 matrix cores that reads them.

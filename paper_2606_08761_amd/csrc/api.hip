@@ -15,6 +15,8 @@ constexpr int kMaxDevices = 64;
 // 0 = unknown, 1 = gfx950, -1 = other architecture.
 std::atomic<int> g_arch_ok[kMaxDevices];
 
+constexpr int64_t kMaxChannelK = 65536;
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 int check_device() {
@@ -34,7 +36,7 @@ int check_device() {
 
 // Shape rules shared by the GEMM entry points.
 int check_gemm_shape(int64_t M, int64_t N, int64_t K) {
-    if (M < 0 || N < 1 || K < 128 || (K % 128) != 0) return APEX4_ERR_SHAPE;
+    if (M < 0 || N < 1 || K < 32 || (K % 32) != 0) return APEX4_ERR_SHAPE;
     if (M > 0x7FFFFFFF || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
     // the kernels address a packed operand row by row with 32-bit byte offsets
     if (M * (K / 2) > 0xFFFFFFFFll || N * (K / 2) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
@@ -43,7 +45,9 @@ int check_gemm_shape(int64_t M, int64_t N, int64_t K) {
 
 int check_gemm_group(int64_t K, int64_t G) {
     if (G <= 0) return APEX4_ERR_GROUP;
-    if (G == K) return APEX4_OK;
+    // one group per row: the kernels hold 256 P of the whole row in one int32,
+    // exact while 2^14 K < 2^31 with room for the split sums
+    if (G == K) return K <= kMaxChannelK ? APEX4_OK : APEX4_ERR_GROUP;
     if (G != 32 && G != 64 && G != 128 && G != 256 && G != 512 && G != 1024) return APEX4_ERR_GROUP;
     if (K % G != 0) return APEX4_ERR_SHAPE;
     return APEX4_OK;
@@ -54,7 +58,7 @@ bool present(const void* p, int64_t rows) { return p != nullptr || rows == 0; }
 
 int check_quant_args(const void* x, int64_t M, int64_t K, int64_t G, const void* A_q, const void* s_a) {
     if (!present(x, M) || !present(A_q, M) || !present(s_a, M)) return APEX4_ERR_NULL;
-    if (M < 0 || K < 128 || (K % 128) != 0 || M > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (M < 0 || K < 32 || (K % 32) != 0 || M > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
     if (G <= 0 || (G % 32) != 0 || G > K) return APEX4_ERR_GROUP;
     if (K % G != 0) return APEX4_ERR_SHAPE;
     if (!aligned16(x) || !aligned16(A_q) || !aligned16(s_a)) return APEX4_ERR_ALIGN;
@@ -91,7 +95,7 @@ const char* apex4_status_string(int status) {
     }
 }
 
-int apex4_version(void) { return 100; }
+int apex4_version(void) { return 200; }
 
 int apex4_quantize_act(const void* x, int64_t M, int64_t K, int64_t G, uint8_t* A_q, void* s_a,
                        void* stream) {
@@ -114,7 +118,7 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, con
     if (M == 0) return APEX4_OK;
     hipError_t e = apex4::launch_gemm(A_q, static_cast<const uint16_t*>(s_a), W_q,
                                       static_cast<const uint16_t*>(s_w), M, N, K, G, static_cast<uint16_t*>(Y),
-                                      nullptr, static_cast<hipStream_t>(stream));
+                                      static_cast<hipStream_t>(stream));
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 
@@ -130,6 +134,38 @@ int apex4_w4a4_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int64_t G, i
     return APEX4_OK;
 }
 
+namespace {
+
+// The dispatch of apex4_w4a4_gemm (workspace == NULL) or apex4_w4a4_gemm_ws,
+// with an optional dump of exact group sums and the general-tile switch.
+int gemm_dispatch(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N,
+                  int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes, apex4::Dump dump,
+                  bool general, void* stream) {
+    const auto sa = static_cast<const uint16_t*>(s_a);
+    const auto sw = static_cast<const uint16_t*>(s_w);
+    const auto y = static_cast<uint16_t*>(Y);
+    const auto st = static_cast<hipStream_t>(stream);
+    const int64_t need = workspace ? apex4::splitk_workspace_bytes(M, N, K, G) : 0;
+    hipError_t e;
+    if (need == 0) {
+        e = apex4::launch_gemm(A_q, sa, W_q, sw, M, N, K, G, y, st, dump, general);
+    } else {
+        if (workspace_bytes < need) return APEX4_ERR_WORKSPACE;
+        e = apex4::launch_gemm_splitk(A_q, sa, W_q, sw, M, N, K, G, y, static_cast<float*>(workspace), st, dump,
+                                      general);
+    }
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int check_window(int64_t M, int64_t m0, int64_t mr, const void* P) {
+    if (!present(P, mr)) return APEX4_ERR_NULL;
+    if (m0 < 0 || mr < 0 || m0 > M || mr > M - m0) return APEX4_ERR_SHAPE;
+    if (!aligned16(P)) return APEX4_ERR_ALIGN;
+    return APEX4_OK;
+}
+
+}  // namespace
+
 int apex4_w4a4_gemm_ws(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
                        int64_t N, int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes,
                        void* stream) {
@@ -139,18 +175,8 @@ int apex4_w4a4_gemm_ws(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, 
     rc = check_device();
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
-    const int64_t need = apex4::splitk_workspace_bytes(M, N, K, G);
-    hipError_t e;
-    if (need == 0) {
-        e = apex4::launch_gemm(A_q, static_cast<const uint16_t*>(s_a), W_q, static_cast<const uint16_t*>(s_w), M, N,
-                               K, G, static_cast<uint16_t*>(Y), nullptr, static_cast<hipStream_t>(stream));
-    } else {
-        if (!workspace || workspace_bytes < need) return APEX4_ERR_WORKSPACE;
-        e = apex4::launch_gemm_splitk(A_q, static_cast<const uint16_t*>(s_a), W_q, static_cast<const uint16_t*>(s_w),
-                                      M, N, K, G, static_cast<uint16_t*>(Y), static_cast<float*>(workspace),
-                                      static_cast<hipStream_t>(stream));
-    }
-    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+    if (!workspace && apex4::splitk_workspace_bytes(M, N, K, G) > 0) return APEX4_ERR_WORKSPACE;
+    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, workspace, workspace_bytes, apex4::Dump(), false, stream);
 }
 
 int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M, int64_t N, int64_t K,
@@ -160,42 +186,118 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M,
     if (rc) return rc;
     rc = check_gemm_group(K, G);
     if (rc) return rc;
-    if (m0 < 0 || mr < 0 || m0 > M || mr > M - m0) return APEX4_ERR_SHAPE;
-    const uint8_t* A_win = A_q + m0 * (K / 2);
-    if (!aligned16(A_q) || !aligned16(W_q) || !aligned16(P) || !aligned16(A_win)) return APEX4_ERR_ALIGN;
+    rc = check_window(M, m0, mr, P);
+    if (rc) return rc;
+    if (!aligned16(A_q) || !aligned16(W_q)) return APEX4_ERR_ALIGN;
     rc = check_device();
     if (rc) return rc;
     if (mr == 0) return APEX4_OK;
-    hipError_t e = apex4::launch_gemm(A_win, nullptr, W_q, nullptr, mr, N, K, G, nullptr, P,
-                                      static_cast<hipStream_t>(stream));
-    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+    // the full M x N problem through apex4_w4a4_gemm's kernel choice, without
+    // scales (no Y): only the window's sums are written
+    const apex4::Dump dump{P, static_cast<int>(m0), static_cast<int>(mr)};
+    return gemm_dispatch(A_q, nullptr, W_q, nullptr, M, N, K, G, nullptr, nullptr, 0, dump, false, stream);
 }
 
-int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
-                      int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, void* stream) {
-    if (!present(x, M) || !W_q || !s_w || !present(Y, M) || !present(A_q_work, M) || !present(s_a_work, M))
-        return APEX4_ERR_NULL;
-    int rc = check_gemm_args(A_q_work, s_a_work, W_q, s_w, M, N, K, G, Y);
+int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
+                          int64_t N, int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes,
+                          int64_t m0, int64_t mr, int32_t* P, int flags, void* stream) {
+    if (!present(P, mr)) return APEX4_ERR_NULL;
+    int rc = check_gemm_args(A_q, s_a, W_q, s_w, M, N, K, G, Y);
     if (rc) return rc;
-    rc = check_quant_args(x, M, K, G, A_q_work, s_a_work);
+    if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
+    if (flags & ~APEX4_DEBUG_GENERAL_TILES) return APEX4_ERR_SHAPE;
+    rc = check_window(M, m0, mr, P);
     if (rc) return rc;
     rc = check_device();
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
+    const apex4::Dump dump{mr > 0 ? P : nullptr, static_cast<int>(m0), static_cast<int>(mr)};
+    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, workspace, workspace_bytes, dump,
+                         (flags & APEX4_DEBUG_GENERAL_TILES) != 0, stream);
+}
+
+namespace {
+
+int linear_dispatch(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K, int64_t G,
+                    void* Y, uint8_t* A_q_work, void* s_a_work, apex4::Dump dump, void* stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const auto xh = static_cast<const uint16_t*>(x);
+    const auto sw = static_cast<const uint16_t*>(s_w);
+    const auto sa = static_cast<uint16_t*>(s_a_work);
+    const auto y = static_cast<uint16_t*>(Y);
     if (apex4::fused_linear_fits(M, N, K, G)) {
-        const hipError_t e = apex4::launch_linear_fused(static_cast<const uint16_t*>(x), W_q, static_cast<const uint16_t*>(s_w),
-                                                        M, N, K, G, static_cast<uint16_t*>(Y), A_q_work,
-                                                        static_cast<uint16_t*>(s_a_work), st);
+        const hipError_t e = apex4::launch_linear_fused(xh, W_q, sw, M, N, K, G, y, A_q_work, sa, st, dump);
         return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
     }
-    hipError_t e = apex4::launch_quantize(static_cast<const uint16_t*>(x), M, K, G, A_q_work,
-                                          static_cast<uint16_t*>(s_a_work), st);
+    hipError_t e = apex4::launch_quantize(xh, M, K, G, A_q_work, sa, st);
     if (e != hipSuccess) return APEX4_ERR_LAUNCH;
-    e = apex4::launch_gemm(A_q_work, static_cast<const uint16_t*>(s_a_work), W_q,
-                           static_cast<const uint16_t*>(s_w), M, N, K, G, static_cast<uint16_t*>(Y), nullptr,
-                           st);
+    e = apex4::launch_gemm(A_q_work, sa, W_q, sw, M, N, K, G, y, st, dump);
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int check_linear_args(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K, int64_t G,
+                      const void* Y, const uint8_t* A_q_work, const void* s_a_work) {
+    if (!present(x, M) || !W_q || !s_w || !present(Y, M) || !present(A_q_work, M) || !present(s_a_work, M))
+        return APEX4_ERR_NULL;
+    const int rc = check_gemm_args(A_q_work, s_a_work, W_q, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    return check_quant_args(x, M, K, G, A_q_work, s_a_work);
+}
+
+}  // namespace
+
+int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
+                      int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, void* stream) {
+    int rc = check_linear_args(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), stream);
+}
+
+int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
+                            int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, int64_t m0, int64_t mr, int32_t* P,
+                            void* stream) {
+    if (!present(P, mr)) return APEX4_ERR_NULL;
+    int rc = check_linear_args(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work);
+    if (rc) return rc;
+    rc = check_window(M, m0, mr, P);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const apex4::Dump dump{mr > 0 ? P : nullptr, static_cast<int>(m0), static_cast<int>(mr)};
+    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, dump, stream);
+}
+
+int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, int flags, int* kernel,
+                         int* splits) {
+    if (!kernel || !splits) return APEX4_ERR_NULL;
+    int rc = check_gemm_shape(M, N, K);
+    if (rc) return rc;
+    rc = check_gemm_group(K, G);
+    if (rc) return rc;
+    if (entry < APEX4_ENTRY_GEMM || entry > APEX4_ENTRY_LINEAR) return APEX4_ERR_SHAPE;
+    if (flags & ~APEX4_DEBUG_GENERAL_TILES) return APEX4_ERR_SHAPE;
+    if (entry == APEX4_ENTRY_LINEAR && flags) return APEX4_ERR_SHAPE;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) {
+        *kernel = 0;
+        *splits = 0;
+        return APEX4_OK;
+    }
+    if (entry == APEX4_ENTRY_LINEAR && apex4::fused_linear_fits(M, N, K, G)) {
+        *kernel = apex4::kKernelFused;
+        *splits = 1;
+        return APEX4_OK;
+    }
+    const apex4::GemmPlan plan =
+        apex4::plan_gemm(M, N, K, G, entry == APEX4_ENTRY_GEMM_WS, (flags & APEX4_DEBUG_GENERAL_TILES) != 0);
+    *kernel = plan.kernel;
+    *splits = plan.splits;
+    return APEX4_OK;
 }
 
 int apex4_pack_fp6(const uint8_t* q4, int64_t rows, int64_t K, uint8_t* q6, void* stream) {

@@ -52,11 +52,18 @@
 //     dequant phases half a stage apart (described at the kernel).  Small tiles
 //     (64 x 128) may split K over two wave groups (KSPLIT) and keep PF stages
 //     of loads in flight.
-//   * Split-K across workgroups (launch_gemm_splitk, G == 128, caller
-//     workspace): when the 128 x 256 tiles leave CUs idle, the ping-pong kernel
-//     runs on a tiles x S grid, each workgroup over S-th of the stages, and
-//     writes its fp32 partial tile; splitk_reduce_kernel adds the S partials
+//   * Split-K across workgroups (launch_gemm_splitk, caller workspace): when
+//     the tiles leave CUs idle, the kernel runs on a tiles x S grid, each
+//     workgroup over S-th of the stages (whole groups), and writes its partial
+//     tile (fp32; exact int32 for G == K); a second kernel adds the S partials
 //     in range order and rounds once.
+//   * K % 128 != 0 (K % 32 == 0; G in {32, 64} or G == K): the last stage is
+//     partial.  Its loads are masked to the row's end (lanes past it hold
+//     zero codes, which add nothing) and its missing groups are skipped.
+//   * Dump (tests and diagnostics): the same kernels, instantiated with DUMP,
+//     also write the exact group sums of a row window, taken from the int32
+//     MFMA results before dequantization; the kernel choice (plan_gemm) is the
+//     one the production call makes.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -81,7 +88,6 @@ enum Mode : int {
     kRotate = 0,    // G <= 128: whole groups per stage
     kPersist = 1,   // G in {256, 512, 1024}: group sums persist over the stages of a group
     kChannel = 2,   // G == K: one scale per row and column, applied in the epilogue
-    kDump = 3,      // exact integer group sums written out (debug)
 };
 
 template <int BM, int NT, int GPS>
@@ -125,11 +131,19 @@ __device__ __forceinline__ i32x16 splat16(int v) {
 // K-group kg runs the contiguous stages [kg nks/KSPLIT, (kg+1) nks/KSPLIT)
 // with LDS buffers of its own, in step with the others (shared barriers); at
 // the end the groups' partial tiles are added through LDS in a fixed order.
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF, int KSPLIT>
+//
+// DUMP: the kernel also writes the exact group sums of rows [pm0, pm0 + pmr)
+// to P[pmr][N][K/G] as each group completes (the Y path is unchanged; with
+// sa == nullptr the scales are not read and Y is not written).
+//
+// K need not be a multiple of 128 (groups of 32 or 64, or G = K): the last
+// stage is then partial, and its missing codes load as zeros, which add
+// nothing to any sum; its missing groups are neither dequantized nor dumped.
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF, int KSPLIT, bool DUMP>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P, int nks_split, void* __restrict__ part) {
+    int32_t* __restrict__ P, int pm0, int pmr, int nks_split, void* __restrict__ part) {
     constexpr int NT = 64 * WAVES_M * WAVES_N;
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     constexpr int A_CH = BM * 4 / NT;                 // 16-byte packed activation chunks per thread
@@ -139,10 +153,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     constexpr int KPG = KK / GPS;                     // MFMAs per group and block
     static_assert(A_CH * NT == BM * 4, "tile / thread mismatch");
     static_assert(BM + BN <= NT, "one staged scale per thread");
-    static_assert(!FINE || MODE == kRotate || MODE == kDump, "fine groups rotate or dump");
-
-    static_assert(KSPLIT == 1 || MODE != kDump, "group sums are dumped per group, K is not split");
+    static_assert(!FINE || MODE == kRotate, "fine groups rotate");
     __shared__ Stage<BM, NT, GPS> st[2][KSPLIT];
+    const bool have_sc = !DUMP || sa != nullptr;  // uniform
 
     // ---- tile selection (XCD-aware) ----
     // Workgroup b runs on XCD b & 7 (round-robin dispatch), each XCD with its
@@ -179,19 +192,22 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     // nks_split stages from blockIdx.y * nks_split (split-K across workgroups)
     const int nks = nks_split / KSPLIT;
     const int kbase = static_cast<int>(blockIdx.y) * nks_split + kg * nks;
-    const int spg = FINE ? 1 : G / KS;  // stages per group
+    // stages per group (per-channel: one group over all stages)
+    const int spg = FINE ? 1 : (MODE == kChannel ? (1 << 30) : G / KS);
     const int ng = K / G;
+    const int kb = K / 2;  // packed bytes per row
 
     // ---- per-lane offsets (32-bit); uniform stage bases live in scalar registers.
     // Rows past M or N are clamped to the last row: they only feed outputs that
     // are never stored, so loads need no branch.
     uint32_t a_off[A_CH];
-    int a_lds0[A_CH], a_lds1[A_CH];
+    int a_lds0[A_CH], a_lds1[A_CH], a_pos[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
         const int c = tid + i * NT;
         const int r = c >> 2, p = c & 3;
         a_off[i] = static_cast<uint32_t>(min(m0 + r, M - 1)) * static_cast<uint32_t>(K / 2) + p * 16;
+        a_pos[i] = 16 * p;  // byte of the chunk within a stage
         if constexpr (FINE) {
             // packed bytes 16p .. 16p+7 and 16p+8 .. 16p+15 are MFMA p, lane halves 0 and 1
             a_lds0[i] = r * AROW + (2 * p) * 16;
@@ -227,23 +243,40 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     auto load_a = [&](int ks, auto SLOT) __attribute__((always_inline)) {
         constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Aq + static_cast<int64_t>(ks) * (KS / 2);
+        const int lim = kb - ks * (KS / 2);  // packed bytes of this stage inside the row (uniform)
+        if (lim >= KS / 2) {
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) ra[sl][i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
-        if constexpr (MODE != kDump) {
-            // the GPS groups of a stage are adjacent in a scale row (K / G is a multiple of GPS)
-            const uint16_t* sp = sc_base + sc_off + static_cast<uint32_t>(ks / spg) * GPS;
+            for (int i = 0; i < A_CH; ++i) ra[sl][i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < A_CH; ++i)
+                ra[sl][i] = a_pos[i] < lim ? *reinterpret_cast<const uint4*>(base + a_off[i]) : make_uint4(0u, 0u, 0u, 0u);
+        }
+        if (have_sc) {
+            // the GPS groups of a stage are adjacent in a scale row.  When ng is
+            // a multiple of GPS every stage is whole and the row's scales are
+            // aligned for one vector load; otherwise (K % 128 != 0) they are
+            // read one by one, and past the last group (partial last stage)
+            // they read as zero.
+            const int g0 = (ks / spg) * GPS;
+            const uint16_t* sp = sc_base + sc_off + static_cast<uint32_t>(g0);
             if constexpr (GPS == 1) {
                 rsc[sl][0] = *sp;
-            } else if constexpr (GPS == 2) {
-                const uint32_t v = *reinterpret_cast<const uint32_t*>(sp);
-                rsc[sl][0] = static_cast<uint16_t>(v);
-                rsc[sl][1] = static_cast<uint16_t>(v >> 16);
+            } else if ((ng % GPS) == 0) {
+                if constexpr (GPS == 2) {
+                    const uint32_t v = *reinterpret_cast<const uint32_t*>(sp);
+                    rsc[sl][0] = static_cast<uint16_t>(v);
+                    rsc[sl][1] = static_cast<uint16_t>(v >> 16);
+                } else {
+                    const uint2 v = *reinterpret_cast<const uint2*>(sp);
+                    rsc[sl][0] = static_cast<uint16_t>(v.x);
+                    rsc[sl][1] = static_cast<uint16_t>(v.x >> 16);
+                    rsc[sl][2] = static_cast<uint16_t>(v.y);
+                    rsc[sl][3] = static_cast<uint16_t>(v.y >> 16);
+                }
             } else {
-                const uint2 v = *reinterpret_cast<const uint2*>(sp);
-                rsc[sl][0] = static_cast<uint16_t>(v.x);
-                rsc[sl][1] = static_cast<uint16_t>(v.x >> 16);
-                rsc[sl][2] = static_cast<uint16_t>(v.y);
-                rsc[sl][3] = static_cast<uint16_t>(v.y >> 16);
+#pragma unroll
+                for (int gi = 0; gi < GPS; ++gi) rsc[sl][gi] = g0 + gi < ng ? sp[gi] : static_cast<uint16_t>(0);
             }
         }
     };
@@ -254,29 +287,34 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
             *reinterpret_cast<i32x4*>(&st[buf][kg].a[a_lds0[i]]) = frag2(ra[sl][i].x, ra[sl][i].y);
             *reinterpret_cast<i32x4*>(&st[buf][kg].a[a_lds1[i]]) = frag2(ra[sl][i].z, ra[sl][i].w);
         }
-        if constexpr (MODE != kDump) {
 #pragma unroll
-            for (int gi = 0; gi < GPS; ++gi) st[buf][kg].scale[gi][tid] = rsc[sl][gi];
-        }
+        for (int gi = 0; gi < GPS; ++gi) st[buf][kg].scale[gi][tid] = rsc[sl][gi];
     };
     // w[slot][j][kk / 2] holds the two packed dwords of MFMA kk (x, y for even kk, z, w for odd)
     uint4 w[PF][NJ][2];
     auto load_w = [&](int ks, auto SLOT) __attribute__((always_inline)) {
         constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2);
+        const int lim = kb - ks * (KS / 2);  // uniform
+        const bool full = lim >= KS / 2;
+        const uint2 z2 = make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             if constexpr (FINE) {
                 // MFMA kk, lane half h: packed bytes 16 kk + 8 h .. + 7
-                const uint2 q0 = *reinterpret_cast<const uint2*>(base + w_off[j]);
-                const uint2 q1 = *reinterpret_cast<const uint2*>(base + w_off[j] + 16);
-                const uint2 q2 = *reinterpret_cast<const uint2*>(base + w_off[j] + 32);
-                const uint2 q3 = *reinterpret_cast<const uint2*>(base + w_off[j] + 48);
+                const uint8_t* q = base + w_off[j];
+                const int h8 = 8 * lh;
+                const uint2 q0 = (full || h8 < lim) ? *reinterpret_cast<const uint2*>(q) : z2;
+                const uint2 q1 = (full || 16 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 16) : z2;
+                const uint2 q2 = (full || 32 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 32) : z2;
+                const uint2 q3 = (full || 48 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 48) : z2;
                 w[sl][j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
                 w[sl][j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
             } else {
-                w[sl][j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
-                w[sl][j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + 16);
+                const int h32 = 32 * lh;
+                w[sl][j][0] = (full || h32 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j]) : make_uint4(0u, 0u, 0u, 0u);
+                w[sl][j][1] = (full || h32 + 16 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j] + 16)
+                                                       : make_uint4(0u, 0u, 0u, 0u);
             }
         }
     };
@@ -325,9 +363,26 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         }
     };
 
-    // One K stage: widen this wave's weight fragments, issue the next stage's
-    // weight loads into the freed registers, then run the row blocks.
-    auto compute = [&](int buf, int next, auto FIRST, auto SLOT) __attribute__((always_inline)) {
+    // Exact group sums of block (i, j) for group g into the dump window
+    // (d holds 256 P, biased by 1.5 * 2^23 when MAGIC_OK).
+    auto dump_block = [&](const i32x16& d, int i, int j, int g) __attribute__((always_inline)) {
+        if constexpr (DUMP) {
+            const int gm = m0 + wm * MI * 32 + i * 32 + l32;
+            if (g < ng && gm >= pm0 && gm < pm0 + pmr) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                    const int v = MAGIC_OK ? (d[r] - static_cast<int>(MAGIC_BITS)) : d[r];
+                    if (gn < N) P[(static_cast<int64_t>(gm - pm0) * N + gn) * ng + g] = v >> 8;
+                }
+            }
+        }
+    };
+
+    // One K stage (global stage index gks): widen this wave's weight fragments,
+    // issue the next stage's weight loads into the freed registers, then run
+    // the row blocks.
+    auto compute = [&](int buf, int next, int gks, auto FIRST, auto SLOT) __attribute__((always_inline)) {
         constexpr bool group_first = decltype(FIRST)::value;
         constexpr int sl = decltype(SLOT)::value;
         i32x4 bw[NJ][KK];
@@ -363,20 +418,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
 #pragma unroll
                 for (int kk = 0; kk < KK; ++kk)
                     d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][kk], af[i & 1][kk], d, 0, 0, 0);
-                if constexpr (ROTATE) dequant(d, acc[i][j], sav[i], swh[j]);
-                else psum[i][j] = d;
+                if constexpr (ROTATE) {
+                    dump_block(d, i, j, gks);
+                    dequant(d, acc[i][j], sav[i], swh[j]);
+                } else {
+                    psum[i][j] = d;
+                }
             }
-        }
-    };
-
-    // Exact group sums of block (i, j) for group g (dump mode).
-    auto dump_block = [&](const i32x16& d, int i, int j, int g) {
-        const int gm = m0 + wm * MI * 32 + i * 32 + l32;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-            const int v = MAGIC_OK ? (d[r] - static_cast<int>(MAGIC_BITS)) : d[r];
-            if (gm < M && gn < N) P[(static_cast<int64_t>(gm) * N + gn) * ng + g] = v >> 8;
         }
     };
 
@@ -410,7 +458,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
             constexpr int f = decltype(F)::value;
             constexpr int gi = f / MI, i = f % MI;
             if constexpr (f + 1 < NF) read_f(f + 1, af[(f + 1) & 1]);
-            if constexpr (MODE == kRotate && i == 0) {
+            if constexpr (i == 0) {
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) read_sw(buf, j, swh[j], gi);
             }
@@ -420,13 +468,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
 #pragma unroll
                 for (int q = 0; q < KPG; ++q)
                     d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][gi * KPG + q], af[f & 1][q], d, 0, 0, 0);
-                if constexpr (MODE == kRotate) dequant(d, acc[i][j], read_sa(buf, i, gi), swh[j]);
-                else dump_block(d, i, j, ks * GPS + gi);
+                dump_block(d, i, j, ks * GPS + gi);
+                dequant(d, acc[i][j], read_sa(buf, i, gi), swh[j]);
             }
         });
     };
 
-    // End of a group for the persistent modes.
+    // End of a group for the persistent mode.
     auto finish_group = [&](int buf, int g) __attribute__((always_inline)) {
         if constexpr (MODE == kPersist) {
 #pragma unroll
@@ -434,20 +482,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
                 uint2 swh[4];
                 read_sw(buf, j, swh);
 #pragma unroll
-                for (int i = 0; i < MI; ++i) dequant(psum[i][j], acc[i][j], read_sa(buf, i), swh);
-            }
-        } else if constexpr (MODE == kDump) {
-#pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int gm = m0 + wm * MI * 32 + i * 32 + l32;
-#pragma unroll
-                for (int j = 0; j < NJ; ++j)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int gn = n0 + wn * NJ * 32 + j * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-                        const int v = MAGIC_OK ? (psum[i][j][r] - static_cast<int>(MAGIC_BITS)) : psum[i][j][r];
-                        if (gm < M && gn < N) P[(static_cast<int64_t>(gm) * N + gn) * ng + g] = v >> 8;
-                    }
+                for (int i = 0; i < MI; ++i) {
+                    dump_block(psum[i][j], i, j, g);
+                    dequant(psum[i][j], acc[i][j], read_sa(buf, i), swh);
+                }
             }
         }
         (void)buf;
@@ -466,11 +504,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         if constexpr (FINE) {
             compute_fine(buf, ahead, kbase + ks, SLOT);
         } else if constexpr (ROTATE) {
-            compute(buf, ahead, std::true_type{}, SLOT);
+            compute(buf, ahead, kbase + ks, std::true_type{}, SLOT);
         } else {
             // a K-group's stages start on a group boundary (nks is a multiple of spg)
-            if ((ks % spg) == 0) compute(buf, ahead, std::true_type{}, SLOT);
-            else compute(buf, ahead, std::false_type{}, SLOT);
+            if ((ks % spg) == 0) compute(buf, ahead, kbase + ks, std::true_type{}, SLOT);
+            else compute(buf, ahead, kbase + ks, std::false_type{}, SLOT);
             if (MODE != kChannel && (ks + 1) % spg == 0) finish_group(buf, (kbase + ks) / spg);
         }
         store_a(buf ^ 1, std::integral_constant<int, (sl + 1) % PF>{});
@@ -494,8 +532,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         constexpr int u = decltype(S)::value;
         if (ks + u < nks) step(ks + u, std::integral_constant<int, u & 1>{}, std::integral_constant<int, u % PF>{});
     });
-
-    if constexpr (MODE == kDump) return;
 
     // ---- K-groups 1 .. KSPLIT-1 hand their partial tiles to group 0, which adds
     // them in group order (fp32 sums, or the exact int32 sums of kChannel)
@@ -527,6 +563,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
                         else acc[i][j][r] += __int_as_float(v);
                     }
     }
+
+    if constexpr (MODE == kChannel) {
+        if (!part) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) dump_block(psum[i][j], i, j, 0);
+        }
+    }
+    if (!have_sc) return;  // group sums only
 
     // ---- epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3.
     // The last step stored a copy of the final stage (and its scales) into the
@@ -629,12 +675,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
 //     free: weights of stage s + 1 right after stage s's are widened, its A
 //     chunk of stage s + 2 right after stage s + 1's is stored (two slots of
 //     cover each).
+//   * DUMP: the group sums of rows [pm0, pm0 + pmr) also go to P[pmr][N][K/128]
+//     in the dequant phase (sa == nullptr: no scales read, no Y written).
+template <bool DUMP>
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y, int nks_split,
-    float* __restrict__ part) {
+    float* __restrict__ part, int32_t* __restrict__ P, int pm0, int pmr) {
     constexpr int NT = 512, BM = 128, BN = 256, MI = 4;
     __shared__ Stage<BM, NT, 1> st[2];
+    const bool have_sc = !DUMP || sa != nullptr;  // uniform
 
     // tile selection: as the kernel above
     const int mt_count = (M + BM - 1) / BM;
@@ -682,7 +732,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     auto load_a = [&](int ks) __attribute__((always_inline)) {
         ks = min(ks, nks - 1) + kofs;
         ra = *reinterpret_cast<const uint4*>(Aq + static_cast<int64_t>(ks) * (KS / 2) + a_off);
-        rsc = sc_base[sc_off + static_cast<uint32_t>(ks)];
+        rsc = have_sc ? sc_base[sc_off + static_cast<uint32_t>(ks)] : static_cast<uint16_t>(0);
     };
     auto store_a = [&](int buf) __attribute__((always_inline)) {
         *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0]) = frag2(ra.x, ra.y);
@@ -746,10 +796,24 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
         });
         __builtin_amdgcn_sched_group_barrier(0x008, LA, 0);
     };
-    // acc += fl(P s_a) * s_w for the four blocks of the last MFMA phase
-    auto dequant_phase = [&]() __attribute__((always_inline)) {
+    // acc += fl(P s_a) * s_w for the four blocks of the last MFMA phase (stage s)
+    auto dequant_phase = [&](int s) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(D[i]));
+        if constexpr (DUMP) {
+            const int g = kofs + s;
+#pragma unroll
+            for (int i = 0; i < MI; ++i) {
+                const int gm = m0 + i * 32 + l32;
+                if (gm >= pm0 && gm < pm0 + pmr) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int gn = n0 + wave * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+                        if (gn < N) P[(static_cast<int64_t>(gm - pm0) * N + gn) * ng + g] = (D[i][r] - static_cast<int>(MAGIC_BITS)) >> 8;
+                    }
+                }
+            }
+        }
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
             const float nb = -MAGIC * sav[i];
@@ -797,7 +861,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
         for (int i = 0; i < MI; ++i) pin(D[i]);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
-        dequant_phase();
+        dequant_phase(s);
 #pragma unroll
         for (int i = 0; i < MI; ++i) pin(acc[i]);
         stage_next(s + ahead);
@@ -805,6 +869,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
         __syncthreads();
     }
     if (!grp_y) __syncthreads();
+    if (!have_sc) return;  // group sums only
 
     // epilogue: lane holds row m and columns 8q + 4h + (0..3), q = 0..3.
     // Split K: the fp32 partial tile goes to part[split][m][n] instead.
@@ -855,9 +920,9 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     }
 }
 
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT>
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT, bool DUMP>
 hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                    int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
+                    int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
                     void* part = nullptr) {
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
@@ -867,10 +932,10 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
     // M = 64..256, N = 8192 for G in {128, 256}, 24 % for G = K).  With G < 128
     // the deeper ring costs occupancy and time, so those keep one stage.
     constexpr int PF = (WAVES_M * WAVES_N * MI * NJ <= 8 && GPS == 1) ? 4 : 1;
-    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT>),
+    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT, DUMP>),
                        dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(64 * WAVES_M * WAVES_N * KSPLIT),
                        0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
-                       static_cast<int>(G), Y, P, static_cast<int>(K / KS / S), part);
+                       static_cast<int>(G), Y, dump.P, dump.m0, dump.mr, static_cast<int>(kstages(K) / S), part);
     return hipGetLastError();
 }
 
@@ -882,21 +947,55 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
 // fit twice, and the split loses (N = 10240: 9 % slower).
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
 hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                  int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
+                  int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
                   void* part = nullptr) {
     constexpr bool small = WAVES_M * WAVES_N * MI * NJ <= 8;
+    if (dump.P) {
+        if (S > 1)
+            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
+                                                                                    stream, S, part);
+        if constexpr (small) {
+            constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
+            const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+            const int64_t stages = kstages(K);
+            const int64_t spg = (MODE == kChannel || GPS > 1) ? 1 : G / KS;
+            if (tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0)
+                return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, true>(Aq, sa, Wq, sw, M, N, K, G, Y,
+                                                                                        dump, stream);
+        }
+        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
+                                                                                stream);
+    }
     if (S > 1)  // split across workgroups: one wave group per workgroup
-        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S,
-                                                                          part);
-    if constexpr (small && MODE != kDump) {
+        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
+                                                                                 stream, S, part);
+    if constexpr (small) {
         constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
         const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-        const int64_t stages = K / KS;
+        const int64_t stages = kstages(K);
         const int64_t spg = (MODE == kChannel || GPS > 1) ? 1 : G / KS;
         if (tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0)
-            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
+                                                                                     stream);
     }
-    return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+    return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
+}
+
+// The G = 128 ping-pong kernel on 128 x 256 tiles (S > 1: split over K, fp32
+// partial tiles to part).
+hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                     int64_t N, int64_t K, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1, float* part = nullptr) {
+    const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(tiles), static_cast<unsigned>(S));
+    const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), nks = static_cast<int>(K / KS / S);
+    if (dump.P)
+        hipLaunchKernelGGL(w4a4_gemm_pp_kernel<true>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
+                           dump.P, dump.m0, dump.mr);
+    else
+        hipLaunchKernelGGL(w4a4_gemm_pp_kernel<false>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
+                           static_cast<int32_t*>(nullptr), 0, 0);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -904,35 +1003,23 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
 // Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  When that
 // tiling would not give every CU a workgroup, 64 x 128 tiles with 4 waves of
 // 64 x 32 (four times as many workgroups, two per CU), or 8 waves splitting K
-// (see launch).  One row goes to the dot-product kernel and up to 32 rows
-// (decode) to the streaming kernel instead, except for the debug dump.
+// (see launch).  G = 128 on 128 x 256 tiles is the ping-pong kernel unless
+// force_general.
 template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                        int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P, hipStream_t stream, int S = 1,
-                        void* part = nullptr) {
-    if (P) {
-        if (G == 32) return launch<1, WAVES_N, MI, 1, kDump, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-        if (G == 64) return launch<1, WAVES_N, MI, 1, kDump, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-        if (G <= 256) return launch<1, WAVES_N, MI, 1, kDump, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-        return launch<1, WAVES_N, MI, 1, kDump, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    }
-    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
-    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
-    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+                        int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
+                        void* part = nullptr, bool force_general = false) {
+    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
     if (G == 128) {
         if constexpr (WAVES_N == 8 && MI == 4) {
-            if (S > 1) return hipErrorInvalidValue;
-            const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
-            if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
-            hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles)), dim3(512), 0, stream, Aq, sa, Wq,
-                               sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
-                               static_cast<int>(K / KS), static_cast<float*>(nullptr));
-            return hipGetLastError();
+            if (!force_general) return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, stream, S, static_cast<float*>(part));
         }
-        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
     }
-    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
-    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream, S, part);
+    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
 }
 
 namespace {
@@ -971,20 +1058,29 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 // Per-channel split-K: the S planes hold exact int32 sums of 256 P; their sum
 // is scaled exactly as the per-channel epilogue does, so Y is the same bits as
 // without the split.
+// With a dump, the exact per-channel group sum (P = the planes' sum / 256) of
+// rows [pm0, pm0 + pmr) also goes to P[pmr][N].
 __global__ __launch_bounds__(256) void splitk_reduce_channel_kernel(const int32_t* __restrict__ part, int S, int M,
                                                                     int N, const uint16_t* __restrict__ sa,
                                                                     const uint16_t* __restrict__ sw,
-                                                                    uint16_t* __restrict__ Y) {
+                                                                    uint16_t* __restrict__ Y, int32_t* __restrict__ P,
+                                                                    int pm0, int pmr) {
     const int64_t MN = static_cast<int64_t>(M) * N;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < MN; i += stride) {
         int32_t p = part[i];
         for (int sp = 1; sp < S; ++sp) p += part[sp * MN + i];
         const int64_t m = i / N, n = i - m * N;
+        if (P && m >= pm0 && m < pm0 + pmr) P[(m - pm0) * N + n] = p >> 8;
         const float sav = h2f(sa[m]) * (1.0f / 256.0f);
         const float v = static_cast<float>(p) * sav * h2f(sw[n]);
         Y[i] = __half_as_ushort(__float2half_rn(v));
     }
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
 }  // namespace
@@ -1004,7 +1100,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_channel_kernel(const int32_
 int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G) {
     if (M <= 0 || gemv_fits(M, N, K, G) || decode_fits(M, N, K, G)) return 1;
     const int64_t cus = device_cu_count();
-    const int64_t nks = K / KS;
+    const int64_t nks = kstages(K);
     if (((M + 127) / 128) * ((N + 255) / 256) >= cus) return 1;
     int S = 1;
     if (G == 128) {
@@ -1034,41 +1130,74 @@ hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* 
     return hipGetLastError();
 }
 
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    const int64_t need = (n + 255) / 256;
+    const int blocks = static_cast<int>(need < 8192 ? need : 8192);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks), dim3(256), 0, stream, p, n, v);
+    return hipGetLastError();
+}
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile) {
+    if (split) {
+        const int S = splitk_factor(M, N, K, G);
+        if (S > 1) return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile64, S};
+    }
+    if (!force_tile && gemv_fits(M, N, K, G)) return {kKernelGemv, 1};
+    if (!force_tile && decode_fits(M, N, K, G)) return {kKernelDecode, 1};
+    const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
+    if (big_tiles < device_cu_count()) return {kKernelTile64, 1};
+    return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile128, 1};
+}
+
+namespace {
+
+hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
+                          const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y,
+                          hipStream_t stream, Dump dump, float* part) {
+    switch (plan.kernel) {
+        case kKernelGemv: return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump);
+        case kKernelDecode: return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump);
+        case kKernelTile64: return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, plan.splits, part);
+        case kKernelTile128:
+            return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, 1, nullptr, /*force_general=*/true);
+        case kKernelPingPong: return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, stream, plan.splits, part);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
-                              hipStream_t stream) {
-    const int S = splitk_factor(M, N, K, G);
-    if (S < 2) return launch_gemm(Aq, sa, Wq, sw, M, N, K, G, Y, nullptr, stream);
-    hipError_t e;
-    if (G == 128) {
-        const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
-        hipLaunchKernelGGL(w4a4_gemm_pp_kernel, dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(512),
-                           0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K), Y,
-                           static_cast<int>(K / KS / S), part);
-        e = hipGetLastError();
-    } else {
-        e = launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, nullptr, stream, S, part);
-    }
+                              hipStream_t stream, Dump dump, bool force_tile) {
+    const GemmPlan plan = plan_gemm(M, N, K, G, true, force_tile);
+    if (plan.splits < 2) return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, nullptr);
+    const int S = plan.splits;
+    // split ranges hold whole groups, so every group sum except the
+    // per-channel one is dumped by the kernel that completes it
+    Dump tile_dump = dump;
+    if (G == K) tile_dump.P = nullptr;
+    const hipError_t e = launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, tile_dump, part);
     if (e != hipSuccess) return e;
     if (G == K) {
         const int64_t need = (M * N + 255) / 256;
         const int blocks = static_cast<int>(need < 8192 ? need : 8192);
         hipLaunchKernelGGL(splitk_reduce_channel_kernel, dim3(blocks), dim3(256), 0, stream,
                            reinterpret_cast<const int32_t*>(part), S, static_cast<int>(M), static_cast<int>(N), sa, sw,
-                           Y);
+                           Y, dump.P, dump.m0, dump.mr);
         return hipGetLastError();
     }
     return launch_splitk_reduce(part, S, M * N, Y, stream);
 }
 
+// One row: the dot-product kernel; up to 32 rows: the weight-streaming kernel;
+// otherwise the tile kernels (the same choice with or without a dump).
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
-                       int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, int32_t* P,
-                       hipStream_t stream) {
-    if (!P && gemv_fits(M, N, K, G)) return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
-    if (!P && decode_fits(M, N, K, G)) return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
-    const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
-    if (big_tiles < device_cu_count()) return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
-    return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, P, stream);
+                       int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump,
+                       bool force_tile) {
+    return launch_planned(plan_gemm(M, N, K, G, false, force_tile), Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump,
+                          nullptr);
 }
 
 }  // namespace apex4

@@ -30,6 +30,13 @@
 //     dequantized with that group's scales.
 //   * The 8 partial fp32 tiles are summed through LDS in a fixed order and
 //     rounded once to binary16.
+//   * K need not be a multiple of 128 (G in {32, 64} or G = K): the last stage
+//     is then partial and its missing codes load as zeros; its missing groups
+//     are skipped.
+//   * DUMP: each stage's exact partial group sums of rows [pm0, pm0 + pmr) are
+//     added with integer atomics into the zeroed P[pmr][N][K/G] (the sum over a
+//     group's stages is exact in any order); sa == nullptr skips the scales
+//     and Y.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -66,10 +73,12 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
 // are dequantized and reduced.  PF: stages in flight per wave.  GPS: groups per
 // 128-wide stage (1 for G >= 128, 2 for G = 64, 4 for G = 32).  Lane l holds
 // rows 8 (r / 4) + 4 (l / 32) + r % 4 for r < MROWS / 2.
-template <int MROWS, int PF, int GPS>
+template <int MROWS, int PF, int GPS, bool DUMP>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
-    const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y) {
+    const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
+    int32_t* __restrict__ P, int pm0, int pmr) {
+    const bool have_sc = !DUMP || sa != nullptr;  // uniform
     constexpr int NR = MROWS / 2;      // output registers per lane that matter
     __shared__ float red[NWAVE][NR][64];
     // [K/G][32] twice: activation scale of row r and group g at g * 32 + r, then
@@ -79,7 +88,8 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int l32 = lane & 31, lh = lane >> 5;
-    const int nks = K / 128;
+    const int nks = (K + 127) / 128;  // the last stage may be partial
+    const int kb = K / 2;
     const int ng = K / G;
     // group of stage s (GPS == 1): s >> lg; first group of stage s (GPS > 1): s * GPS
     const int lg = (G == K) ? 31 : (G <= 128 ? 0 : (G == 256 ? 1 : (G == 512 ? 2 : 3)));
@@ -191,15 +201,21 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     int lt = 0, li = 0;
     // 32 packed bytes of one lane for a stage: two 16-byte runs (GPS == 1), or
     // four 8-byte pieces 16 apart (one per MFMA) when groups are finer than a stage
-    auto load32 = [](const uint8_t* p, uint4 (&r)[2]) __attribute__((always_inline)) {
+    // lim: packed bytes of the stage inside the row (64 unless it is the partial
+    // last stage); pieces past it load as zeros
+    auto load32 = [&](const uint8_t* p, uint4 (&r)[2], int lim) __attribute__((always_inline)) {
+        const bool full = lim >= 64;
         if constexpr (GPS == 1) {
-            r[0] = *reinterpret_cast<const uint4*>(p);
-            r[1] = *reinterpret_cast<const uint4*>(p + 16);
+            const int h = static_cast<int>(HOFF) * lh;
+            r[0] = (full || h < lim) ? *reinterpret_cast<const uint4*>(p) : make_uint4(0u, 0u, 0u, 0u);
+            r[1] = (full || h + 16 < lim) ? *reinterpret_cast<const uint4*>(p + 16) : make_uint4(0u, 0u, 0u, 0u);
         } else {
-            const uint2 q0 = *reinterpret_cast<const uint2*>(p);
-            const uint2 q1 = *reinterpret_cast<const uint2*>(p + 16);
-            const uint2 q2 = *reinterpret_cast<const uint2*>(p + 32);
-            const uint2 q3 = *reinterpret_cast<const uint2*>(p + 48);
+            const int h = static_cast<int>(HOFF) * lh;
+            const uint2 z = make_uint2(0u, 0u);
+            const uint2 q0 = (full || h < lim) ? *reinterpret_cast<const uint2*>(p) : z;
+            const uint2 q1 = (full || h + 16 < lim) ? *reinterpret_cast<const uint2*>(p + 16) : z;
+            const uint2 q2 = (full || h + 32 < lim) ? *reinterpret_cast<const uint2*>(p + 32) : z;
+            const uint2 q3 = (full || h + 48 < lim) ? *reinterpret_cast<const uint2*>(p + 48) : z;
             r[0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
             r[1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
         }
@@ -208,8 +224,9 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const int s = min(wave + NWAVE * li, nks - 1);
         const uint8_t* wb = Wq + static_cast<int64_t>(s) * 64;
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
-        load32(wb + w_voff, rw[j]);
-        load32(ab + a_voff, ra[j]);
+        const int lim = kb - s * 64;
+        load32(wb + w_voff, rw[j], lim);
+        load32(ab + a_voff, ra[j], lim);
         if (++li == per_tile) {
             if (lt + 1 < my_tiles) {
                 li = 0;
@@ -234,12 +251,15 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     // activation scales of rows 0 .. 31 (rows past M clamped) and the first
     // tile's weight scales, their loads in flight together
     const int c0 = tile_col0(0);
-    if (my_tiles > 0) stage(sa, M - 1, sas, sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
-    else stage(sa, M - 1, sas, nullptr, 0, nullptr);
-    if (pf_sc && my_tiles > 1) prefetch_wscales(1);
+    if (have_sc) {
+        if (my_tiles > 0) stage(sa, M - 1, sas, sw + static_cast<int64_t>(c0) * ng, N - 1 - c0, wsc);
+        else stage(sa, M - 1, sas, nullptr, 0, nullptr);
+        if (pf_sc && my_tiles > 1) prefetch_wscales(1);
+    }
     __syncthreads();  // activation scales and the first tile's weight scales staged
 
     int pi = 0;  // stage-in-tile of the next processed stage
+    int pt = 0;  // tile of the next processed stage
     auto process = [&](int j) {
         const int s_raw = wave + NWAVE * pi;
         const bool live = s_raw < nks;
@@ -261,6 +281,20 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
             for (int q = 0; q < KPG; ++q)
                 d = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[gi * KPG + q], bw[gi * KPG + q], d, 0, 0, 0);
+            if (g >= ng) continue;  // past the last group (partial last stage)
+            if constexpr (DUMP) {
+                const int col = tile_col0(pt) + l32;
+                if (live && col < N) {
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) {
+                        const int row = 8 * (r >> 2) + 4 * lh + (r & 3);
+                        if (row >= pm0 && row < pm0 + pmr)
+                            atomicAdd(&P[(static_cast<int64_t>(row - pm0) * N + col) * ng + g],
+                                      (d[r] - static_cast<int>(MAGIC_BITS)) >> 8);
+                    }
+                }
+                if (!have_sc) continue;
+            }
             const float s1 = live ? h2f(wsc[g * ROWS + l32]) * (1.0f / 256.0f) : 0.f;
             const float nb = -MAGIC * s1;
             uint2 sah[4];
@@ -283,7 +317,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
         for (int r = 0; r < NR; ++r) red[wave][r][lane] = acc[r];
         __syncthreads();
-        if (t + 1 < my_tiles) {
+        if (have_sc && t + 1 < my_tiles) {
             if (pf_sc) store_wscales();
             else stage_wscales(t + 1);
         }
@@ -295,14 +329,13 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
             for (int w = 0; w < NWAVE; ++w) v += red[w][r][ln];
             const int row = 8 * (r >> 2) + 4 * (ln >> 5) + (r & 3);
             const int col = n0 + (ln & 31);
-            if (row < M && col < N) Y[static_cast<int64_t>(row) * N + col] = __half_as_ushort(__float2half_rn(v));
+            if (have_sc && row < M && col < N) Y[static_cast<int64_t>(row) * N + col] = __half_as_ushort(__float2half_rn(v));
         }
         __syncthreads();
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[r] = 0.f;
     };
 
-    int pt = 0;
     for (int q0 = 0; q0 < total; q0 += PF) {
 #pragma unroll
         for (int j = 0; j < PF; ++j) {
@@ -312,21 +345,21 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
                 if (++pi == per_tile) {
                     finish_tile(pt++);
                     pi = 0;
-                    if (pf_sc && pt + 1 < my_tiles) prefetch_wscales(pt + 1);
+                    if (have_sc && pf_sc && pt + 1 < my_tiles) prefetch_wscales(pt + 1);
                 }
             }
         }
     }
 }
 
-template <int PF, int GPS>
+template <int PF, int GPS, bool DUMP>
 hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                            int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+                            int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream) {
     static bool lds_attr_set = false;  // benign race: every caller sets the same value
     if (!lds_attr_set) {
-        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS>)}) {
+        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS, DUMP>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS, DUMP>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS, DUMP>)}) {
             const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * MAX_SC_LDS);
             if (e != hipSuccess) return e;
         }
@@ -338,12 +371,25 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
     if (M <= 8)
-        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
+                           dump.P, dump.m0, dump.mr);
     else if (M <= 16)
-        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
+                           dump.P, dump.m0, dump.mr);
     else
-        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y);
+        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
+                           dump.P, dump.m0, dump.mr);
     return hipGetLastError();
+}
+
+template <int PF, int GPS>
+hipError_t launch_decode_g(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                           int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream) {
+    if (!dump.P) return launch_decode_pf<PF, GPS, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
+    // partial sums are added atomically into a zeroed window
+    const hipError_t e = launch_fill_i32(dump.P, static_cast<int64_t>(dump.mr) * N * (K / G), 0, stream);
+    if (e != hipSuccess) return e;
+    return launch_decode_pf<PF, GPS, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
 }
 
 }  // namespace
@@ -367,12 +413,12 @@ bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
-                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+                              int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump) {
     if (!decode_fits(M, N, K, G)) return hipErrorInvalidValue;
     // four group sums per stage hold more registers: a shorter ring keeps G = 32 spill-free
-    if (G == 32) return launch_decode_pf<DECODE_PF - 2, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
-    if (G == 64) return launch_decode_pf<DECODE_PF, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
-    return launch_decode_pf<DECODE_PF, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, stream);
+    if (G == 32) return launch_decode_g<DECODE_PF - 2, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
+    if (G == 64) return launch_decode_g<DECODE_PF, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
+    return launch_decode_g<DECODE_PF, 1>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
 }
 
 }  // namespace apex4

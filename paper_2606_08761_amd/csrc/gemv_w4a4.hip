@@ -27,6 +27,9 @@
 //     instead of its codes and quantizes it into LDS in the prologue with the
 //     quantizer's own arithmetic (quant_core.h: same codes and scales, bit for
 //     bit); workgroup 0 also writes them to the caller's work buffers.
+//   * DUMP (pmr == 1): every lane's exact 32-code partial sum is added with an
+//     integer atomic into the zeroed P[1][N][K/G], giving the exact group sums
+//     whatever the order; sa == nullptr (codes only) skips the scales and Y.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -56,11 +59,13 @@ __device__ __forceinline__ float wave_sum(float v) {
 // n0 = (b * GV_WAVES + w) * rpw, and walks its (row, chunk) pairs row-major in
 // batches of GV_LOADS loads.  lgG: log2(G), or 31 for G = K (one group).
 // QL = G / 8: slots of 8 values per group (FUSE only).
-template <bool FUSE, int QL>
+template <bool FUSE, int QL, bool DUMP>
 __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int N, int K, int G, int lgG, int rpw, uint16_t* __restrict__ Y,
-    const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out) {
+    const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out,
+    int32_t* __restrict__ P, int pmr) {
+    const bool have_sc = FUSE || !DUMP || sa != nullptr;  // uniform
     // A's codes (K/2 bytes), then s_a as binary32 [K/G]
     extern __shared__ uint4 gv_lds[];
     const int tid = threadIdx.x, lane = tid & 63;
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
             const int off = c * GV_CHUNK + 16 * lane;
             const bool ok = f0 + j < units && n < N && off < kb;
             w[j] = ok ? *reinterpret_cast<const uint4*>(Wq + static_cast<int64_t>(n) * kb + off) : make_uint4(0u, 0u, 0u, 0u);
-            sws[j] = ok ? sw[static_cast<int64_t>(n) * ng + ((2 * off) >> lgG)] : static_cast<uint16_t>(0);
+            sws[j] = (ok && have_sc) ? sw[static_cast<int64_t>(n) * ng + ((2 * off) >> lgG)] : static_cast<uint16_t>(0);
             if (++c == nch) {
                 c = 0;
                 ++r;
@@ -137,7 +142,8 @@ __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
         }
     } else {
         for (int i = tid; i < kb / 16; i += GV_NT) gv_lds[i] = reinterpret_cast<const uint4*>(Aq)[i];
-        for (int i = tid; i < ng; i += GV_NT) sa_lds[i] = gv_h2f(sa[i]);
+        if (have_sc)
+            for (int i = tid; i < ng; i += GV_NT) sa_lds[i] = gv_h2f(sa[i]);
     }
     __syncthreads();
     if (n0 >= N) return;  // after the only barrier
@@ -156,13 +162,19 @@ __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
                     p = __builtin_amdgcn_sdot8(static_cast<int>(a.y), static_cast<int>(w[j].y), p, false);
                     p = __builtin_amdgcn_sdot8(static_cast<int>(a.z), static_cast<int>(w[j].z), p, false);
                     p = __builtin_amdgcn_sdot8(static_cast<int>(a.w), static_cast<int>(w[j].w), p, false);
-                    const float t = static_cast<float>(p) * sa_lds[(2 * off) >> lgG];
-                    acc = fmaf(t, gv_h2f(sws[j]), acc);
+                    if constexpr (DUMP) {
+                        const int n = n0 + r;
+                        if (pmr > 0 && n < N) atomicAdd(&P[static_cast<int64_t>(n) * ng + ((2 * off) >> lgG)], p);
+                    }
+                    if (have_sc) {
+                        const float t = static_cast<float>(p) * sa_lds[(2 * off) >> lgG];
+                        acc = fmaf(t, gv_h2f(sws[j]), acc);
+                    }
                 }
                 if (c == nch - 1) {  // row n0 + r complete (uniform)
                     const float s = wave_sum(acc);
                     const int n = n0 + r;
-                    if (lane == 0 && n < N) Y[n] = __half_as_ushort(__float2half_rn(s));
+                    if (have_sc && lane == 0 && n < N) Y[n] = __half_as_ushort(__float2half_rn(s));
                     acc = 0.f;
                 }
             }
@@ -194,15 +206,25 @@ GemvGrid gemv_grid(int64_t N, int64_t K) {
 template <bool FUSE, int QL>
 hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t N,
                          int64_t K, int64_t G, uint16_t* Y, const uint16_t* x, uint8_t* aq_out, uint16_t* sa_out,
-                         hipStream_t stream) {
+                         Dump dump, hipStream_t stream) {
     const GemvGrid gg = gemv_grid(N, K);
     int lgG = 31;
     if (G != K)
         for (lgG = 5; (int64_t{1} << lgG) < G; ++lgG) {
         }
-    hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL>), dim3(static_cast<unsigned>(gg.grid)), dim3(GV_NT),
-                       gemv_lds_bytes(K, G), stream, Aq, sa, Wq, sw, static_cast<int>(N), static_cast<int>(K),
-                       static_cast<int>(G), lgG, static_cast<int>(gg.rpw), Y, x, aq_out, sa_out);
+    const dim3 gd(static_cast<unsigned>(gg.grid)), bd(GV_NT);
+    const size_t lds = gemv_lds_bytes(K, G);
+    const int n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G), rpw = static_cast<int>(gg.rpw);
+    if (dump.P) {
+        // 32-code partial sums are added atomically into a zeroed window
+        const hipError_t e = launch_fill_i32(dump.P, static_cast<int64_t>(dump.mr) * N * (K / G), 0, stream);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL, true>), gd, bd, lds, stream, Aq, sa, Wq, sw, n, k, g, lgG, rpw, Y, x,
+                           aq_out, sa_out, dump.P, dump.mr);
+    } else {
+        hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL, false>), gd, bd, lds, stream, Aq, sa, Wq, sw, n, k, g, lgG, rpw, Y,
+                           x, aq_out, sa_out, static_cast<int32_t*>(nullptr), 0);
+    }
     return hipGetLastError();
 }
 
@@ -214,9 +236,9 @@ bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
 }
 
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream) {
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump) {
     if (!gemv_fits(M, N, K, G)) return hipErrorInvalidValue;
-    return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, stream);
+    return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, dump, stream);
 }
 
 // Every workgroup quantizes all of x, so the fused prologue's total work is
@@ -231,16 +253,16 @@ bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
 }
 
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N, int64_t K,
-                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream) {
+                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream, Dump dump) {
     if (!fused_linear_fits(M, N, K, G)) return hipErrorInvalidValue;
     const uint8_t* no_aq = nullptr;
     const uint16_t* no_sa = nullptr;
     switch (G) {
-        case 32: return launch_gemv_t<true, 4>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
-        case 64: return launch_gemv_t<true, 8>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
-        case 128: return launch_gemv_t<true, 16>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
-        case 256: return launch_gemv_t<true, 32>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
-        default: return launch_gemv_t<true, 64>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, stream);
+        case 32: return launch_gemv_t<true, 4>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
+        case 64: return launch_gemv_t<true, 8>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
+        case 128: return launch_gemv_t<true, 16>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
+        case 256: return launch_gemv_t<true, 32>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
+        default: return launch_gemv_t<true, 64>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
     }
 }
 

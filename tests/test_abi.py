@@ -35,8 +35,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums",
-              "apex4_w4a4_linear", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
+    for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
+              "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
               "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
               "apex4_w4a4_gemm_mx_ws", "apex4_status_string", "apex4_version"):
         assert f in names
@@ -58,7 +58,7 @@ def test_status_strings(L):
         assert L.apex4_status_string(code).decode().startswith(name)
     assert L.apex4_status_string(-7).decode().startswith("APEX4_ERR_WORKSPACE")
     assert L.apex4_status_string(12345)
-    assert L.apex4_version() >= 100
+    assert L.apex4_version() >= 200
 
 
 class Host:
@@ -85,8 +85,13 @@ def test_quantize_validation(L):
     assert q(h.ptr(), 4, 256, 128, NULL, h.ptr(), s) == -1
     assert q(h.ptr(), 4, 256, 128, h.ptr(), NULL, s) == -1
     assert q(h.ptr(), -1, 256, 128, h.ptr(), h.ptr(), s) == -2
-    assert q(h.ptr(), 4, 96, 32, h.ptr(), h.ptr(), s) == -2        # K % 128
+    assert q(h.ptr(), 4, 80, 16, h.ptr(), h.ptr(), s) == -2        # K % 32
+    assert q(h.ptr(), 4, 16, 16, h.ptr(), h.ptr(), s) == -2        # K < 32
     assert q(h.ptr(), 4, 0, 128, h.ptr(), h.ptr(), s) == -2
+    # K % 32 == 0 and any G % 32 == 0 dividing K pass the shape and group
+    # rules: the misaligned x is the first error
+    for K, G in ((32, 32), (96, 32), (96, 96), (160, 160), (8224, 32), (480, 160), (65568, 65568)):
+        assert q(h.ptr(8), 4, K, G, h.ptr(), h.ptr(), s) == -4, (K, G)
     assert q(h.ptr(), 4, 256, 48, h.ptr(), h.ptr(), s) == -3       # G % 32
     assert q(h.ptr(), 4, 256, 512, h.ptr(), h.ptr(), s) == -3      # G > K
     assert q(h.ptr(), 4, 384, 256, h.ptr(), h.ptr(), s) == -2      # K % G
@@ -105,8 +110,17 @@ def test_gemm_validation(L):
     assert g(*ok, 4, 8, 256, 128, NULL, s) == -1
     assert g(*ok, -1, 8, 256, 128, h.ptr(), s) == -2
     assert g(*ok, 4, 0, 256, 128, h.ptr(), s) == -2
-    assert g(*ok, 4, 8, 64, 64, h.ptr(), s) == -2                  # K < 128
-    assert g(*ok, 4, 8, 320, 64, h.ptr(), s) == -2                 # K % 128
+    assert g(*ok, 4, 8, 16, 16, h.ptr(), s) == -2                  # K < 32
+    assert g(*ok, 4, 8, 48, 48, h.ptr(), s) == -2                  # K % 32
+    assert g(*ok, 4, 8, 200, 200, h.ptr(), s) == -2
+    # K >= 32, K % 32 == 0 with G in {32, ..., 1024} dividing K or G == K <= 65536
+    # pass the shape and group rules (the misaligned A_q is the first error)
+    for K, G in ((32, 32), (64, 64), (96, 32), (96, 96), (160, 32), (160, 160), (320, 64), (8224, 32),
+                 (8224, 8224), (65536, 65536), (16352, 32)):
+        assert g(h.ptr(1), *ok[1:], 4, 8, K, G, h.ptr(), s) == -4, (K, G)
+    assert g(*ok, 4, 8, 65568, 65568, h.ptr(), s) == -3            # per-channel K above 65536
+    assert g(*ok, 4, 8, 131072, 131072, h.ptr(), s) == -3
+    assert g(*ok, 4, 8, 96, 64, h.ptr(), s) == -2                  # K % G
     assert g(*ok, 4, 8, 384, 96, h.ptr(), s) == -3                 # G not in {32,...,1024} and not K
     assert g(*ok, 4, 8, 4096, 2048, h.ptr(), s) == -3
     assert g(*ok, 4, 8, 1024, 1000, h.ptr(), s) == -3
@@ -129,6 +143,38 @@ def test_groupsums_validation(L):
     assert f(h.ptr(), h.ptr(), 8, 8, 256, 128, 0, 8, h.ptr(4), s) == -4
 
 
+def test_debug_validation(L):
+    h = Host()
+    f = L.apex4_w4a4_gemm_debug
+    s = NULL
+    ok = [h.ptr()] * 4
+    ws = (NULL, 0)
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, NULL, 0, s) == -1       # no P for a window
+    assert f(*ok, 8, 8, 256, 128, NULL, *ws, 0, 8, h.ptr(), 0, s) == -1       # no Y
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 4, 5, h.ptr(), 0, s) == -2    # window past M
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, h.ptr(), 2, s) == -2    # unknown flag
+    assert f(*ok, 8, 8, 256, 96, h.ptr(), *ws, 0, 8, h.ptr(), 0, s) == -3
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, h.ptr(4), 0, s) == -4   # misaligned P
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), h.ptr(8), 1 << 20, 0, 8, h.ptr(), 0, s) == -4
+    g = L.apex4_w4a4_linear_debug
+    args = [h.ptr()] * 3
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, NULL, s) == -1
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 2, 3, h.ptr(), s) == -2
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, h.ptr(8), s) == -4
+
+
+def test_plan_validation(L):
+    f = L.apex4_w4a4_gemm_plan
+    k, sp = ctypes.c_int(-9), ctypes.c_int(-9)
+    assert f(0, 8, 8, 256, 128, 0, None, ctypes.byref(sp)) == -1
+    assert f(0, 8, 8, 48, 48, 0, ctypes.byref(k), ctypes.byref(sp)) == -2
+    assert f(0, 8, 8, 65568, 65568, 0, ctypes.byref(k), ctypes.byref(sp)) == -3
+    assert f(3, 8, 8, 256, 128, 0, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown entry
+    assert f(0, 8, 8, 256, 128, 4, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown flag
+    assert f(2, 8, 8, 256, 128, 1, ctypes.byref(k), ctypes.byref(sp)) == -2   # no flags for the linear
+    assert (k.value, sp.value) == (-9, -9)                                     # nothing written
+
+
 def test_linear_validation(L):
     h = Host()
     f = L.apex4_w4a4_linear
@@ -138,6 +184,7 @@ def test_linear_validation(L):
     assert f(*args(), 4, 8, 256, 128, h.ptr(), NULL, h.ptr(), s) == -1
     assert f(*args(), 4, 8, 200, 128, h.ptr(), h.ptr(), h.ptr(), s) == -2
     assert f(*args(), 4, 8, 384, 96, h.ptr(), h.ptr(), h.ptr(), s) == -3
+    assert f(*args(x=h.ptr(2)), 4, 8, 96, 32, h.ptr(), h.ptr(), h.ptr(), s) == -4   # K = 96 accepted
     assert f(*args(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -4
 
 
@@ -220,6 +267,8 @@ import paper_2606_08761_amd as pk
 L = pk.lib()
 b = np.zeros(1 << 16, np.uint8); p = ctypes.c_void_p((b.ctypes.data + 255) & ~255)
 print(L.apex4_w4a4_gemm(p, p, p, p, 0, 8, 256, 128, p, None))
+k = ctypes.c_int(0)
+print(L.apex4_w4a4_gemm_plan(0, 8, 8, 96, 32, 0, ctypes.byref(k), ctypes.byref(k)))
 """ % ROOT
     try:
         import torch
@@ -229,7 +278,7 @@ print(L.apex4_w4a4_gemm(p, p, p, p, 0, 8, 256, 128, p, None))
         pass
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
     assert out.returncode == 0, out.stderr
-    assert out.stdout.strip().splitlines()[-1] == "-6"
+    assert out.stdout.strip().splitlines()[-2:] == ["-6", "-6"]
 
 
 def test_binding_refuses_host_tensors():
