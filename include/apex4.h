@@ -97,6 +97,29 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a,
                     void* Y, void* stream);
 
 /*
+ * apex4_w4a4_gemm_ws without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same kernels and the same Y, bit for bit,
+ * as apex4_w4a4_gemm_ws; where that call would split K, the partial planes go
+ * to a static device array of APEX4_NOALLOC_SCRATCH_BYTES that the library
+ * holds on each device it runs on until the process ends.  The call itself
+ * allocates nothing (no hipMalloc / hipFree).
+ *
+ *   Arguments and errors as apex4_w4a4_gemm, plus APEX4_ERR_WORKSPACE when the
+ *   shape's split would need more than APEX4_NOALLOC_SCRATCH_BYTES (the size
+ *   query apex4_w4a4_gemm_workspace_size returns that need; on a 256-CU
+ *   MI355X every split fits).
+ *   All calls on one device share its array: calls that may overlap on one
+ *   device (different streams, or host threads) race and must be ordered by
+ *   the caller.  Nothing in the array needs clearing between calls.
+ */
+#define APEX4_NOALLOC_SCRATCH_BYTES (32ll << 20)
+int apex4_w4a4_gemm_noalloc(const uint8_t* A_q, const void* s_a,
+                            const uint8_t* W_q, const void* s_w,
+                            int64_t M, int64_t N, int64_t K, int64_t G,
+                            void* Y, void* stream);
+
+/*
  * Debug form of apex4_w4a4_gemm: the exact integer group sums of Eq.
  * (group_decomposition).  The whole M x N problem runs through the kernel
  * that apex4_w4a4_gemm picks for this shape (one-row, few-row or tile kernel),

@@ -24,13 +24,16 @@ APEX4_OK = 0
 STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
           -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE", -7: "APEX4_ERR_WORKSPACE"}
 APEX4_DEBUG_GENERAL_TILES = 1
+APEX4_NOALLOC_SCRATCH_BYTES = 32 << 20
 ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2}
 KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong"}
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
-            "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size",
-            "apex4_w4a4_gemm_ws", "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
-            "apex4_w4a4_gemm_mx_ws", "apex4_status_string", "apex4_version")
+            "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6",
+            "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
+            "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
+            "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws", "apex4_status_string",
+            "apex4_version")
 
 _lib = None
 
@@ -65,12 +68,13 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm_mx_workspace_size.argtypes = [I, I, I, I, P]
     L.apex4_w4a4_gemm_mx_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_gemm_ws.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
+    L.apex4_w4a4_gemm_noalloc.argtypes = [P, P, P, P, I, I, I, I, P, P]
     L.apex4_w4a4_gemm_fp6.argtypes = [P, P, P, P, I, I, I, I, P, P]
     for f in ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
-              "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug",
-              "apex4_pack_fp6", "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
-              "apex4_quantize_mx", "apex4_w4a4_gemm_mx", "apex4_w4a4_gemm_mx_workspace_size",
-              "apex4_w4a4_gemm_mx_ws"):
+              "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6",
+              "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
+              "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
+              "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -157,6 +161,21 @@ def apex4_w4a4_gemm_ws(A_q, s_a, W_q, s_w, G: int, workspace=None, Y=None, strea
                                   M, N, K, G, _dev(Y, torch.float16, "Y"), _dev(workspace, torch.uint8, "workspace"),
                                   workspace.numel(), _stream(A_q, stream))
     _check("apex4_w4a4_gemm_ws", rc)
+    return Y
+
+
+def apex4_w4a4_gemm_noalloc(A_q, s_a, W_q, s_w, G: int, Y=None, stream=None):
+    """apex4_w4a4_gemm_ws with the library's static per-device scratch in place
+    of a workspace: the C call allocates nothing (Y is made here when None)."""
+    import torch
+    M, K2 = A_q.shape
+    N = W_q.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
+    rc = lib().apex4_w4a4_gemm_noalloc(_dev(A_q, torch.uint8, "A_q"), _dev(s_a, torch.float16, "s_a"),
+                                       _dev(W_q, torch.uint8, "W_q"), _dev(s_w, torch.float16, "s_w"),
+                                       M, N, 2 * K2, G, _dev(Y, torch.float16, "Y"), _stream(A_q, stream))
+    _check("apex4_w4a4_gemm_noalloc", rc)
     return Y
 
 

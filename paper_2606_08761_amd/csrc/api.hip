@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "apex4.h"
 #include "apex4_internal.h"
@@ -90,7 +91,9 @@ const char* apex4_status_string(int status) {
         case APEX4_ERR_ALIGN: return "APEX4_ERR_ALIGN: a pointer is not 16-byte aligned";
         case APEX4_ERR_LAUNCH: return "APEX4_ERR_LAUNCH: kernel launch failed";
         case APEX4_ERR_DEVICE: return "APEX4_ERR_DEVICE: no gfx950 device is current";
-        case APEX4_ERR_WORKSPACE: return "APEX4_ERR_WORKSPACE: workspace NULL or too small";
+        case APEX4_ERR_WORKSPACE:
+            return "APEX4_ERR_WORKSPACE: workspace NULL or too small (apex4_w4a4_gemm_noalloc: the split needs more "
+                   "than its static scratch)";
         default: return "APEX4: unknown status";
     }
 }
@@ -196,6 +199,56 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M,
     // scales (no Y): only the window's sums are written
     const apex4::Dump dump{P, static_cast<int>(m0), static_cast<int>(mr)};
     return gemm_dispatch(A_q, nullptr, W_q, nullptr, M, N, K, G, nullptr, nullptr, 0, dump, false, stream);
+}
+
+}  // extern "C"
+
+// Split-K partial planes of apex4_w4a4_gemm_noalloc.  Each device holds its own
+// copy for the life of the process; host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device (the name itself
+// is a host-side stand-in, not a device address).
+static __device__ __align__(256) uint8_t scratch[APEX4_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+void* g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// This device's `scratch`, looked up once per device with that device current.
+int scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return APEX4_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return APEX4_ERR_LAUNCH;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return APEX4_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int apex4_w4a4_gemm_noalloc(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
+                            int64_t N, int64_t K, int64_t G, void* Y, void* stream) {
+    int rc = check_gemm_args(A_q, s_a, W_q, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    const int64_t need = apex4::splitk_workspace_bytes(M, N, K, G);
+    if (need > APEX4_NOALLOC_SCRATCH_BYTES) return APEX4_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if (need > 0) {
+        rc = scratch_address(&ws);
+        if (rc) return rc;
+    }
+    // every partial plane element is written before the reduce reads it: the
+    // scratch needs no clearing
+    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, ws, need, apex4::Dump(), false, stream);
 }
 
 int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,

@@ -227,6 +227,18 @@ def test_workspace_validation(L):
     assert g(*ok, 4, 8, 256, 128, h.ptr(), h.ptr(8), 1 << 20, s) == -4   # misaligned workspace
 
 
+def test_noalloc_validation(L):
+    h = Host()
+    g = L.apex4_w4a4_gemm_noalloc
+    s = NULL
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), s) == -1
+    assert g(*ok, 4, 8, 256, 128, NULL, s) == -1
+    assert g(*ok, 4, 8, 48, 48, h.ptr(), s) == -2
+    assert g(*ok, 4, 8, 256, 96, h.ptr(), s) == -3
+    assert g(*ok, 4, 8, 256, 128, h.ptr(2), s) == -4
+
+
 def test_mx_validation(L):
     h = Host()
     q = L.apex4_quantize_mx

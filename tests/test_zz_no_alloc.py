@@ -1,0 +1,74 @@
+"""apex4_w4a4_gemm_noalloc: the workspace GEMM with the library's static
+per-device scratch in place of a caller workspace (for callers that cannot
+allocate).  Its Y must equal apex4_w4a4_gemm_ws's bit for bit (same kernels,
+same split), and the oracle's within tolerance, on consecutive calls that
+share the scratch, the second with a smaller problem (a stale partial from
+the first call would show up in it).
+"""
+import numpy as np
+import pytest
+
+from parity import check_tolerance, dev, host, log
+from paper_2606_08761_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+# (M, N, K, G): each pair is a larger split then a smaller one.  The first
+# needs the whole scratch on a 256-CU device (4 x 256 x 8192 fp32 partials).
+PAIRS = [
+    ((256, 8192, 8192, 128), (300, 2000, 4096, 128)),
+    ((128, 2048, 8192, 32), (65, 1001, 2048, 32)),
+    ((256, 4096, 8192, 8192), (64, 520, 3072, 3072)),
+    ((300, 2000, 4096, 128), (16, 1024, 4096, 128)),   # then a shape that does not split
+]
+
+
+def _case(O, M, N, K, G, seed):
+    import torch
+    m = pk()
+    r = np.random.default_rng(seed)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+    d = [dev(a) for a in (Aq, sa, Wq, sw)]
+    need = m.apex4_w4a4_gemm_workspace_size(M, N, K, G)
+    assert need <= m.APEX4_NOALLOC_SCRATCH_BYTES
+    plan = m.apex4_w4a4_gemm_plan("gemm_ws", M, N, K, G)
+    log(f"noalloc M={M} N={N} K={K} G={G}: {plan}, workspace {need} bytes")
+    Y = m.apex4_w4a4_gemm_noalloc(*d, G)
+    ws = torch.empty((max(need, 16),), dtype=torch.uint8, device="cuda")
+    Y_ws = m.apex4_w4a4_gemm_ws(*d, G, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Y_ws), (M, N, K, G)
+    rows = np.unique(np.concatenate([np.arange(min(M, 4)), np.arange(M - 2, M), r.integers(0, M, size=6)]))
+    check_tolerance(host(Y)[rows], O.gemm_rows(Aq, sa, Wq, sw, K, G, rows), f"noalloc {M}x{N}x{K} G{G}")
+    return plan
+
+
+def pk():
+    import paper_2606_08761_amd as m
+    return m
+
+
+@pytest.mark.parametrize("first,second", PAIRS)
+def test_noalloc_matches_workspace_entry(O, first, second):
+    p1 = _case(O, *first, seed=sum(first))
+    p2 = _case(O, *second, seed=sum(second) + 1)
+    assert p1[1] > 1
+    if second != (16, 1024, 4096, 128):
+        assert p2[1] > 1
+
+
+def test_noalloc_repeat_and_empty():
+    """Back-to-back calls on one stream give the same bits; M == 0 is a no-op."""
+    import torch
+    m = pk()
+    M, N, K, G = 256, 8192, 8192, 128
+    r = np.random.default_rng(7)
+    d = [dev(a) for a in (wl.random_codes(r, M, K), wl.random_scales(r, M, K // G),
+                          wl.random_codes(r, N, K), wl.random_scales(r, N, K // G))]
+    Y1 = m.apex4_w4a4_gemm_noalloc(*d, G)
+    Y2 = m.apex4_w4a4_gemm_noalloc(*d, G)
+    torch.cuda.synchronize()
+    assert torch.equal(Y1, Y2)
+    m.apex4_w4a4_gemm_noalloc(d[0][:0], d[1][:0], d[2], d[3], G)
+    torch.cuda.synchronize()
