@@ -47,7 +47,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
-    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers", "variants"),
+    p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers", "variants",
+                                      "decode_counters"),
                    default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
@@ -68,6 +69,11 @@ def parse():
     p.add_argument("--power-log", help="summarize: output of --mode power (written to profiles/power_clock_paper_shape.md)")
     p.add_argument("--power-command", default="python3 bench.py --mode power", help="summarize: the command that made --power-log")
     p.add_argument("--layers-log", help="summarize: output of --mode layers (written to profiles/layer_sweep_llama2_70b.md)")
+    p.add_argument("--decode-fetch-csv", help="summarize: counter_collection.csv of the FETCH_SIZE pass over --mode decode_counters")
+    p.add_argument("--decode-write-csv", help="summarize: counter_collection.csv of the WRITE_SIZE pass over --mode decode_counters")
+    p.add_argument("--decode-trace-csv", help="summarize: kernel_trace.csv of the --kernel-trace run of --mode decode_counters")
+    p.add_argument("--decode-log", help="summarize: output of --mode decode_counters (its JSON line)")
+    p.add_argument("--decode-commands", help="summarize: text file with the commands that made the --decode-* files")
     p.add_argument("--layers-command", default="python3 bench.py --mode layers", help="summarize: the command that made --layers-log")
     return p.parse_args()
 
@@ -91,6 +97,18 @@ def traffic_from_profile():
         return float(prof["hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def host_cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(target_s: float, threads: int = 0):
@@ -121,7 +139,7 @@ def cpu_baseline(target_s: float, threads: int = 0):
         dt = (dt * reps + time.perf_counter() - t0) / (reps + 1)
         reps += 1
     tops = 2.0 * rows * N * K / dt / 1e12
-    return {"value": tops, "unit": "TOPS", "cores": O.num_threads(), "kind": "oracle",
+    return {"value": tops, "unit": "TOPS", "cores": O.num_threads(), "kind": "oracle", "cpu": host_cpu_model(),
             "sample": f"{rows} of {M} rows of the M={M} N={N} K={K} G={G} linear "
                       f"(quantize rows + int64/fp64 GEMM rows), mean of {reps} run(s) of {dt:.1f} s"}
 
@@ -145,6 +163,8 @@ def summarize_mode(args):
         xs = [v for k, vs in vals.items() if key in k for v in vs]
         return statistics.mean(xs) if xs else None
 
+    if args.decode_fetch_csv:
+        summarize_decode_traffic(args)
     if not (args.fetch_csv and args.write_csv and args.stats_csv):
         if args.layers_log:
             summarize_layers(args.layers_log, args.layers_command)
@@ -215,12 +235,15 @@ def summarize_mode(args):
                   "graph = the same calls replayed from a captured graph (GPU time, used for GB/s).", "",
                   "Linear = apex4_w4a4_linear from fp16 x (one fused kernel at M=1 where it pays, quantizer + GEMM otherwise); "
                   "quantize then GEMM = the two entry points called in turn.", "",
-                  "| decode M | N | K | linear us (eager / graph) | quantize then GEMM us (graph) | GEMM us (eager / graph) | "
-                  "GEMM HBM GB/s | fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
-                  "|---|---|---|---|---|---|---|---|---|"]
+                  "Weights in the tiled layout; the row-major column runs the same GEMM on row-major weights.", "",
+                  "| decode M | N | K | kernel | linear us (eager / graph) | quantize then GEMM us (graph) | "
+                  "GEMM us (eager / graph) | GEMM HBM GB/s (fraction of 8 TB/s) | row-major GEMM us (graph) | "
+                  "fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
+                  "|---|---|---|---|---|---|---|---|---|---|---|"]
         for d in b.get("decode", []):
-            lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d['linear_us']} / {d.get('linear_graph_us')} | "
-                         f"{d.get('quant_then_gemm_graph_us')} | {d['gemm_us']} / {d.get('gemm_graph_us')} | {d['gemm_hbm_gbs']} | "
+            lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d.get('kernel')} | {d['linear_us']} / {d.get('linear_graph_us')} | "
+                         f"{d.get('quant_then_gemm_graph_us')} | {d['gemm_us']} / {d.get('gemm_graph_us')} | "
+                         f"{d['gemm_hbm_gbs']} ({d['gemm_hbm_frac']}) | {d.get('row_major_gemm_graph_us')} | "
                          f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} / {d.get('speedup_linear_graph_vs_fp16')} |")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -753,7 +776,9 @@ DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)] + [
 
 
 def decode_bench(reps: int = 50):
-    """Decode-size linears (few rows, memory-bound): quantize + GEMM from fp16 x.
+    """Decode-size linears (few rows, memory-bound): quantize + GEMM from fp16 x,
+    with the weights in the tiled layout (what W4A4Linear keeps); the same
+    calls on row-major weights are reported beside them.
 
     Weight copies are rotated past the 256 MB Infinity Cache.  Algorithmic bytes of
     the GEMM: M K/2 + N K/2 + 2 (M + N) K/G + 2 M N; the linear adds the fp16 x
@@ -777,9 +802,11 @@ def decode_bench(reps: int = 50):
             Rw = max(2, -(-ROTATE_BYTES // (Nd * Kd // 2 + 2 * Nd * (Kd // Gd))))
             Rf = max(2, -(-ROTATE_BYTES // (2 * Nd * Kd)))
             wcache.clear()
-            wcache[(Nd, Kd)] = ([(Wq.clone(), sw.clone()) for _ in range(Rw)], [w.clone() for _ in range(Rf)])
-            del w, Wq, sw
-        qsets, fsets = wcache[(Nd, Kd)]
+            Wt = pk.apex4_tile_weights(Wq)
+            wcache[(Nd, Kd)] = ([(Wq.clone(), sw.clone()) for _ in range(Rw)], [w.clone() for _ in range(Rf)],
+                                [Wt.clone() for _ in range(Rw)])
+            del w, Wq, sw, Wt
+        qsets, fsets, tsets = wcache[(Nd, Kd)]
         x = torch.from_numpy(wl.activations(wl.rng_for("decode", 1, Md * 1000 + Nd // 1024), Md, Kd)).to(dev)
         Aq = torch.empty((Md, Kd // 2), dtype=torch.uint8, device=dev)
         sa = torch.empty((Md, Kd // Gd), dtype=torch.float16, device=dev)
@@ -825,12 +852,17 @@ def decode_bench(reps: int = 50):
             del g
             return e0.elapsed_time(e1) / reps * 1e3
 
-        lin = lambda i: pk.apex4_w4a4_linear(x, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y, Aq, sa)
-        gem = lambda i: pk.apex4_w4a4_gemm(Aq, sa, qsets[i % len(qsets)][0], qsets[i % len(qsets)][1], Gd, Y)
+        nq = len(qsets)
+        lin = lambda i: pk.apex4_w4a4_linear_tiled(x, tsets[i % nq], qsets[i % nq][1], Gd, Y, Aq, sa)
+        gem = lambda i: pk.apex4_w4a4_gemm_tiled(Aq, sa, tsets[i % nq], qsets[i % nq][1], Gd, Y=Y)
+        lin_r = lambda i: pk.apex4_w4a4_linear(x, qsets[i % nq][0], qsets[i % nq][1], Gd, Y, Aq, sa)
+        gem_r = lambda i: pk.apex4_w4a4_gemm(Aq, sa, qsets[i % nq][0], qsets[i % nq][1], Gd, Y)
         lin_us = timed(lin)
         gemm_us = timed(gem)
         lin_g_us = graph_timed(lin, Y)
         gemm_g_us = graph_timed(gem, Y)
+        lin_r_g_us = graph_timed(lin_r, Y)
+        gemm_r_g_us = graph_timed(gem_r, Y)
         # the same linear as two kernels (quantizer, then GEMM): what the linear
         # entry point runs unless its one-row fused kernel pays
         two = lambda i: (pk.apex4_quantize_act(x, Gd, Aq, sa), gem(i))
@@ -844,12 +876,152 @@ def decode_bench(reps: int = 50):
                     "gemm_hbm_gbs": round(gbytes / (gemm_g_us * 1e-6) / 1e9, 1),
                     "gemm_hbm_frac": round(gbytes / (gemm_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
                     "linear_hbm_gbs": round((gbytes + 2 * Md * Kd) / (lin_g_us * 1e-6) / 1e9, 1),
+                    "kernel": pk.apex4_w4a4_gemm_plan("linear", Md, Nd, Kd, Gd, pk.APEX4_DEBUG_W_TILED)[0],
+                    "row_major_linear_graph_us": round(lin_r_g_us, 2), "row_major_gemm_graph_us": round(gemm_r_g_us, 2),
+                    "row_major_gemm_hbm_frac": round(gbytes / (gemm_r_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
                     "fp16_gemm_us": round(fp16_us, 2), "speedup_linear_vs_fp16": round(fp16_us / lin_us, 3),
                     "speedup_linear_graph_vs_fp16": round(fp16_us / lin_g_us, 3)})
         del x, Aq, sa, Y, yf
     wcache.clear()
     torch.cuda.synchronize()
     return out
+
+
+# Decode-size linears for per-kernel HBM traffic counters: the memory-bound
+# configuration (M in {1, 8, 32}, N x K = 8192 x 8192 and 28672 x 8192) and the
+# Llama-2-70B linears at M = 16; G = 128.
+DECODE_TRAFFIC = ([("decode", Md, Nd, 8192) for Nd in (8192, 28672) for Md in (1, 8, 32)] +
+                  [("llama70b M=16 qkv", 16, 10240, 8192), ("llama70b M=16 o_proj", 16, 8192, 8192),
+                   ("llama70b M=16 gate_up", 16, 57344, 8192), ("llama70b M=16 down", 16, 8192, 28672)])
+DECODE_TRAFFIC_REPS = 3
+
+
+def decode_counters_mode():
+    """A 256 MiB reference copy 3 times, then each DECODE_TRAFFIC linear
+    (apex4_w4a4_linear_tiled from fp16 x: the fused one-row kernel where it
+    applies, else the quantizer and the GEMM) DECODE_TRAFFIC_REPS times, on
+    tiled weight copies rotated past the 256 MB cache.  All inputs are made
+    first, so the only kernels launched in order are these; the printed launch
+    list maps profiler dispatches to cases."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import rho, workloads as wl
+    dev = torch.device("cuda", 0)
+    Gd = 128
+    src = torch.randint(0, 255, (256 << 20,), dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    cases = []
+    for (label, Md, Nd, Kd) in DECODE_TRAFFIC:
+        w = torch.from_numpy(wl.weights(wl.rng_for("decode", 2, Nd * 3 + Kd // 1024), Nd, Kd)).to(dev)
+        Wq, sw = pk.apex4_quantize_act(w, Gd)
+        # tiled copies rotated past the 256 MB cache (each launch reads weights
+        # no recent launch touched)
+        R = max(2, -(-ROTATE_BYTES // (Nd * Kd // 2)))
+        Wts = [pk.apex4_tile_weights(Wq) for _ in range(R)]
+        del w, Wq
+        x = torch.from_numpy(wl.activations(wl.rng_for("decode", 1, Md * 1000 + Nd // 1024), Md, Kd)).to(dev)
+        bufs = (torch.empty((Md, Nd), dtype=torch.float16, device=dev),
+                torch.empty((Md, Kd // 2), dtype=torch.uint8, device=dev),
+                torch.empty((Md, Kd // Gd), dtype=torch.float16, device=dev))
+        kern, _ = pk.apex4_w4a4_gemm_plan("linear", Md, Nd, Kd, Gd, pk.APEX4_DEBUG_W_TILED)
+        cases.append((label, Md, Nd, Kd, kern, x, Wts, sw, bufs))
+    torch.cuda.synchronize()
+    launches = []
+    for _ in range(3):
+        rho.copy(src, dst)
+        launches.append(("copy", "copy", 256 << 20, 256 << 20))
+    for (label, Md, Nd, Kd, kern, x, Wts, sw, (Y, Aq, sa)) in cases:
+        wbytes = Nd * Kd // 2 + 2 * Nd * (Kd // Gd)
+        for i in range(DECODE_TRAFFIC_REPS):
+            pk.apex4_w4a4_linear_tiled(x, Wts[i % len(Wts)], sw, Gd, Y, Aq, sa)
+            tag = label if label != "decode" else f"decode M={Md} N={Nd} K={Kd}"
+            if kern == "fused":
+                launches.append((tag, "fused", 2 * Md * Kd + wbytes, 2 * Md * Nd + Md * Kd // 2 + 2 * Md * (Kd // Gd)))
+            else:
+                launches.append((tag, "quant", 2 * Md * Kd, Md * Kd // 2 + 2 * Md * (Kd // Gd)))
+                launches.append((tag, kern, Md * Kd // 2 + 2 * Md * (Kd // Gd) + wbytes, 2 * Md * Nd))
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "decode_counters", "G": Gd, "launches": launches}), flush=True)
+
+
+def _decode_kernel_role(name: str):
+    """Role of a profiled dispatch in --mode decode_counters, or None for others."""
+    if "copy_kernel" in name:
+        return "copy"
+    if "quant_small_kernel" in name or "quant_large_kernel" in name:
+        return "quant"
+    if "w4a4_gemv_kernel" in name:
+        return "fused" if re.search(r"w4a4_gemv_kernel<true", name) else "gemv"
+    if "w4a4_decode_kernel" in name:
+        return "decode"
+    if is_tiled_gemm(name):
+        return "tile"
+    return None
+
+
+def summarize_decode_traffic(args):
+    """profiles/decode_traffic.md: HBM bytes per dispatch of the decode-size
+    linears (FETCH_SIZE and WRITE_SIZE, scaled by what they read for the
+    256 MiB reference copy) next to the algorithmic bytes and the kernel-trace
+    durations of the same launches."""
+    import csv
+    import statistics
+    log = json.loads([l for l in open(args.decode_log) if l.startswith("{")][-1])
+    launches = log["launches"]
+
+    def ordered(path, counter=None, name_key="Kernel_Name"):
+        rows = []
+        for r in csv.DictReader(open(path)):
+            if counter and r.get("Counter_Name") != counter:
+                continue
+            role = _decode_kernel_role(r[name_key])
+            if role is None:
+                continue
+            rows.append((int(r.get("Dispatch_Id") or r.get("Correlation_Id") or 0), role, r))
+        rows.sort(key=lambda t: t[0])
+        # set-up (weight quantization) precedes the first reference copy
+        first = next(i for i, t in enumerate(rows) if t[1] == "copy")
+        rows = rows[first:]
+        if [t[1] for t in rows] != [l[1] for l in launches]:
+            raise SystemExit(f"{path}: dispatch roles {[t[1] for t in rows]} differ from the launch list")
+        return [t[2] for t in rows]
+
+    fetch = [float(r["Counter_Value"]) for r in ordered(args.decode_fetch_csv, "FETCH_SIZE")]
+    write = [float(r["Counter_Value"]) for r in ordered(args.decode_write_csv, "WRITE_SIZE")]
+    trace = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in ordered(args.decode_trace_csv)]
+    kib = (256 << 20) / 1024.0
+    fs = kib / statistics.mean(fetch[:3])
+    ws = kib / statistics.mean(write[:3])
+    groups = {}
+    for (tag, role, rb, wb), f, w, us in zip(launches, fetch, write, trace):
+        if role == "copy":
+            continue
+        g = groups.setdefault((tag, role), dict(rb=rb, wb=wb, f=[], w=[], us=[]))
+        g["f"].append(f * fs * 1024.0)
+        g["w"].append(w * ws * 1024.0)
+        g["us"].append(us)
+    cmds = open(args.decode_commands).read().strip() if args.decode_commands else ""
+    lines = ["# Decode-size linears: HBM traffic per kernel (rocprofv3 counters)", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
+             "`bench.py --mode decode_counters` runs a 256 MiB reference copy 3 times, then each linear",
+             "(`apex4_w4a4_linear_tiled` from fp16 x, G = 128: the fused one-row kernel where the library picks",
+             "it, else the quantizer and the GEMM) 3 times, on tiled weight copies rotated past the 256 MB cache.",
+             "FETCH_SIZE and WRITE_SIZE",
+             "(KiB per dispatch) are scaled by what they read for the copy "
+             f"(read scale {fs:.3f}, write scale {ws:.3f}).  Duration: kernel trace of a separate run of the same",
+             "command (mean of the 3 launches; counter runs serialize dispatches).  GB/s = (measured read + write)",
+             "/ duration; algorithmic bytes: codes, scales, fp16 x or Y as the kernel must move them once.", "",
+             "| linear | kernel | algorithmic read MB | HBM read MB | algorithmic write MB | HBM write MB | "
+             "measured / algorithmic | duration us | HBM GB/s | fraction of 8 TB/s |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for (tag, role), g in groups.items():
+        rd, wr, us = statistics.mean(g["f"]), statistics.mean(g["w"]), statistics.mean(g["us"])
+        gbs = (rd + wr) / (us * 1e-6) / 1e9
+        lines.append(f"| {tag} | {role} | {g['rb'] / 1e6:.2f} | {rd / 1e6:.2f} | {g['wb'] / 1e6:.3f} | {wr / 1e6:.3f} | "
+                     f"{(rd + wr) / (g['rb'] + g['wb']):.2f} | {us:.2f} | {gbs:.0f} | {gbs / HBM_PEAK_GBS:.3f} |")
+    with open(os.path.join(ROOT, "profiles", "decode_traffic.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def main():
@@ -866,6 +1038,8 @@ def main():
         return layers_mode()
     if args.mode == "variants":
         return variants_mode()
+    if args.mode == "decode_counters":
+        return decode_counters_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
@@ -891,11 +1065,12 @@ def main():
     sets = []
     w_dev = torch.from_numpy(w_h).to(dev)
     Wq0, sw0 = pk.apex4_quantize_act(w_dev, G)
+    Wt0 = pk.apex4_tile_weights(Wq0)                     # offline weight packing (tiled layout)
     for r in range(R):
         x = torch.from_numpy(x_h).to(dev)
         if r:
             x = x.roll(r, dims=0).contiguous()           # different bytes per set, same distribution
-        sets.append(dict(x=x, Wq=Wq0.clone(), sw=sw0.clone(),
+        sets.append(dict(x=x, Wq=Wq0.clone(), Wt=Wt0.clone(), sw=sw0.clone(),
                          Y=torch.empty((M, N), dtype=torch.float16, device=dev),
                          Aq=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
                          sa=torch.empty((M, K // G), dtype=torch.float16, device=dev)))
@@ -909,7 +1084,7 @@ def main():
         pk.apex4_quantize_act(s["x"], G, s["Aq"], s["sa"])
         if ev is not None:
             ev[1].record(stream)
-        pk.apex4_w4a4_gemm(s["Aq"], s["sa"], s["Wq"], s["sw"], G, s["Y"])
+        pk.apex4_w4a4_gemm_tiled(s["Aq"], s["sa"], s["Wt"], s["sw"], G, Y=s["Y"])
         if ev is not None:
             ev[2].record(stream)
 
@@ -936,17 +1111,28 @@ def main():
     # ---- GEMM alone on the random-code workload (value-independent speed check) ----
     Aq_h, sa_h, Wq_h, sw_h = wl.codes_workload("paper", M, N, K, G)
     c = [torch.from_numpy(a).to(dev) for a in (Aq_h, sa_h, Wq_h, sw_h)]
+    Wt_c = pk.apex4_tile_weights(c[2])
     Yc = torch.empty((M, N), dtype=torch.float16, device=dev)
-    for _ in range(5):
-        pk.apex4_w4a4_gemm(*c, G, Yc)
+    Yt = torch.empty_like(Yc)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     reps = 20
-    e0.record(stream)
-    for _ in range(reps):
-        pk.apex4_w4a4_gemm(*c, G, Yc)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    codes_gemm_ms = e0.elapsed_time(e1) / reps
+
+    def avg_ms(fn):
+        for _ in range(5):
+            fn()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    codes_gemm_ms = avg_ms(lambda: pk.apex4_w4a4_gemm(*c, G, Yc))           # row-major weights
+    codes_gemm_t_ms = avg_ms(lambda: pk.apex4_w4a4_gemm_tiled(c[0], c[1], Wt_c, c[3], G, Y=Yt))
+    rowmajor_step_gemm_ms = avg_ms(lambda: pk.apex4_w4a4_gemm(sets[0]["Aq"], sets[0]["sa"], sets[0]["Wq"],
+                                                              sets[0]["sw"], G, sets[0]["Y"]))
+    tiled_same_bits = bool(torch.equal(Yc, Yt))
+    del Wt_c, Yt
 
     # ---- the same GEMM on the FP6 matrix cores (codes re-encoded as e3m2) ----
     A6, W6 = pk.apex4_pack_fp6(c[0]), pk.apex4_pack_fp6(c[2])
@@ -1038,7 +1224,7 @@ def main():
         "dtype": "int4",
         "data": "synthetic",
         "config": {"workload": "W4A4-g128 linear, paper GEMM shape: quantize fp16 x[2048,8192] "
-                               "(SymQuant, G=128) + W4A4 GEMM against W_q[8192,8192]",
+                               "(SymQuant, G=128) + W4A4 GEMM against W_q[8192,8192] (tiled weight layout)",
                    "M": M, "N": N, "K": K, "G": G, "parallelism": "none (1 GPU)",
                    "mfma": "v_mfma_i32_32x32x32_i8, i32 group sums, fp32 dequant, fp16 out",
                    "rotating_input_sets": R},
@@ -1052,7 +1238,11 @@ def main():
         "gemm_us_p10_p50_p90": [round(float(np.percentile(gemm_all, q)) * 1e3, 3) for q in (10, 50, 90)],
         "gemm_tops": round(gemm_tops, 2),
         "gemm_pct_int8_peak": round(100 * gemm_tops / INT8_PEAK_TOPS, 2),
-        "gemm_random_codes_us": round(codes_gemm_ms * 1e3, 3),
+        "gemm_random_codes_us": round(codes_gemm_t_ms * 1e3, 3),
+        "weights": "tiled layout (apex4_tile_weights, offline)",
+        "gemm_row_major_weights_us": round(rowmajor_step_gemm_ms * 1e3, 3),
+        "gemm_random_codes_row_major_us": round(codes_gemm_ms * 1e3, 3),
+        "tiled_same_bits_as_row_major": tiled_same_bits,
         "fp16_gemm_us": round(fp16_ms * 1e3, 3),
         "fp16_gemm_tflops": round(ops / (fp16_ms * 1e-3) / 1e12, 2),
         "speedup_gemm_vs_fp16": round(fp16_ms / gemm_ms, 3),

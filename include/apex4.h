@@ -133,12 +133,14 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
                               int64_t M, int64_t N, int64_t K, int64_t G,
                               int64_t m0, int64_t mr, int32_t* P, void* stream);
 
-/* flags of apex4_w4a4_gemm_debug */
+/* flags of apex4_w4a4_gemm_debug (and of apex4_w4a4_gemm_plan, apex4_w4a4_linear_debug) */
 #define APEX4_DEBUG_GENERAL_TILES 1 /* tile kernel only: no one-row, few-row or G = 128 ping-pong kernel */
+#define APEX4_DEBUG_W_TILED 2       /* W_q is in the tiled layout of apex4_tile_weights */
 
 /*
- * Debug form of apex4_w4a4_gemm / apex4_w4a4_gemm_ws that returns, from the
- * same launches that compute Y, the exact int32 group sums of Eq.
+ * Debug form of apex4_w4a4_gemm / apex4_w4a4_gemm_ws (and, with
+ * APEX4_DEBUG_W_TILED, apex4_w4a4_gemm_tiled) that returns, from the same
+ * launches that compute Y, the exact int32 group sums of Eq.
  * (group_decomposition) for rows [m0, m0 + mr).
  *
  *   Operands and Y as apex4_w4a4_gemm.  workspace == NULL: the kernel choice
@@ -146,9 +148,11 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
  *   there, including APEX4_ERR_WORKSPACE).
  *   P [mr, N, K/G] int32 (device, output), window as in
  *   apex4_w4a4_gemm_groupsums; mr == 0 writes no sums (P may be NULL).
- *   flags: 0, or APEX4_DEBUG_GENERAL_TILES (other bits: APEX4_ERR_SHAPE).
- * With flags == 0, Y is bit for bit the Y of the production entry point named
- * above.  For tests and diagnostics; slower than the production calls.
+ *   flags: 0 or a combination of APEX4_DEBUG_GENERAL_TILES and
+ *   APEX4_DEBUG_W_TILED (other bits: APEX4_ERR_SHAPE).
+ * Without APEX4_DEBUG_GENERAL_TILES, Y is bit for bit the Y of the production
+ * entry point named above.  For tests and diagnostics; slower than the
+ * production calls.
  */
 int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
                           const uint8_t* W_q, const void* s_w,
@@ -171,12 +175,48 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
  * The GEMM kernel that `entry` runs for this shape on the current device, and
  * its split over K (*splits = S > 1 only for APEX4_ENTRY_GEMM_WS, whose
  * workspace size query then returns S M N 4 bytes).  flags as in
- * apex4_w4a4_gemm_debug (0 for APEX4_ENTRY_LINEAR).  M == 0 gives kernel 0,
+ * apex4_w4a4_gemm_debug (APEX4_DEBUG_W_TILED: the tiled entry points;
+ * APEX4_ENTRY_LINEAR takes no APEX4_DEBUG_GENERAL_TILES).  M == 0 gives kernel 0,
  * splits 0.  Shape and group rules as apex4_w4a4_gemm; unknown entry or flags:
  * APEX4_ERR_SHAPE.  Launches nothing.
  */
 int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, int flags,
                          int* kernel, int* splits);
+
+/*
+ * Tiled weight layout: the offline packing step of the weights (Sec. 4.4
+ * quantizes and packs W once, offline, into the vectors its kernel loads), laid
+ * out for the CDNA4 MFMA fragments: 32-row tiles by 128-wide K stages, and in
+ * each, the 32 packed bytes every lane of a 32-column fragment consumes stored
+ * contiguously in lane order, so that a wave reads its fragment of a stage as
+ * one 2 KB block:
+ *   W_t[t][s][j][l][b] = W_q[32 t + l % 32][64 s + 32 (l / 32) + 16 j + b]
+ *   (t < ceil(N/32), s < ceil(K/128), j < 2, l < 64, b < 16; zero past N and
+ *   past K/2).
+ * apex4_tiled_weights_size writes its size, ceil(N/32) ceil(K/128) 2048 bytes.
+ * apex4_tile_weights writes it from packed codes W_q [N, K/2] (device,
+ * read-only) into W_t (device, output, that size; must not alias W_q).
+ * N >= 1, K >= 32 and K % 32 == 0; W_q and W_t under 4 GiB.
+ */
+int apex4_tiled_weights_size(int64_t N, int64_t K, int64_t* bytes);
+int apex4_tile_weights(const uint8_t* W_q, int64_t N, int64_t K, uint8_t* W_t, void* stream);
+
+/*
+ * apex4_w4a4_gemm / apex4_w4a4_gemm_ws on tiled weights: the same Y, bit for
+ * bit, with W_t from apex4_tile_weights in place of W_q (s_w unchanged).
+ * workspace == NULL: the kernel choice of apex4_w4a4_gemm (no split over K);
+ * otherwise that of apex4_w4a4_gemm_ws (workspace as there).
+ * G in {128, 256, 512, 1024} or G == K >= 128 (APEX4_ERR_GROUP otherwise: the
+ * layout serves kernels that take one group per stage or more); W_t under
+ * 4 GiB; other rules as apex4_w4a4_gemm.
+ * With one row the result is within the tolerance of apex4_w4a4_gemm (the
+ * one-row kernel adds its fp32 partial sums in another order) and otherwise
+ * the same bits.
+ */
+int apex4_w4a4_gemm_tiled(const uint8_t* A_q, const void* s_a,
+                          const uint8_t* W_t, const void* s_w,
+                          int64_t M, int64_t N, int64_t K, int64_t G,
+                          void* Y, void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
  * Quantize-then-GEMM linear layer: the inference forward of one quantized
@@ -197,14 +237,23 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
                       void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
 
 /*
- * Debug form of apex4_w4a4_linear: the same kernels (fused or quantize + GEMM),
- * Y and work buffers bit for bit, plus the exact int32 group sums of rows
+ * apex4_w4a4_linear on tiled weights (apex4_tile_weights): the same kernels'
+ * tiled forms, G and W_t rules as apex4_w4a4_gemm_tiled.
+ */
+int apex4_w4a4_linear_tiled(const void* x, const uint8_t* W_t, const void* s_w,
+                            int64_t M, int64_t N, int64_t K, int64_t G,
+                            void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
+
+/*
+ * Debug form of apex4_w4a4_linear (flags 0) or apex4_w4a4_linear_tiled (flags
+ * APEX4_DEBUG_W_TILED): the same kernels (fused or quantize + GEMM), Y and
+ * work buffers bit for bit, plus the exact int32 group sums of rows
  * [m0, m0 + mr) into P [mr, N, K/G] as in apex4_w4a4_gemm_debug.
  */
 int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w,
                             int64_t M, int64_t N, int64_t K, int64_t G,
                             void* Y, uint8_t* A_q_work, void* s_a_work,
-                            int64_t m0, int64_t mr, int32_t* P, void* stream);
+                            int64_t m0, int64_t mr, int32_t* P, int flags, void* stream);
 
 /*
  * Workspace form of apex4_w4a4_gemm for shapes that leave compute units idle

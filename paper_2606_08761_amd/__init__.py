@@ -24,6 +24,7 @@ APEX4_OK = 0
 STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4_ERR_GROUP",
           -4: "APEX4_ERR_ALIGN", -5: "APEX4_ERR_LAUNCH", -6: "APEX4_ERR_DEVICE", -7: "APEX4_ERR_WORKSPACE"}
 APEX4_DEBUG_GENERAL_TILES = 1
+APEX4_DEBUG_W_TILED = 2
 APEX4_NOALLOC_SCRATCH_BYTES = 32 << 20
 ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2}
 KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong"}
@@ -33,7 +34,8 @@ EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums"
             "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
             "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
             "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws", "apex4_status_string",
-            "apex4_version")
+            "apex4_version", "apex4_tiled_weights_size", "apex4_tile_weights", "apex4_w4a4_gemm_tiled",
+            "apex4_w4a4_linear_tiled")
 
 _lib = None
 
@@ -60,7 +62,11 @@ def lib() -> ctypes.CDLL:
     L.apex4_w4a4_gemm_debug.argtypes = [P, P, P, P, I, I, I, I, P, P, I, I, I, P, ctypes.c_int, P]
     L.apex4_w4a4_gemm_plan.argtypes = [ctypes.c_int, I, I, I, I, ctypes.c_int, P, P]
     L.apex4_w4a4_linear.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
-    L.apex4_w4a4_linear_debug.argtypes = [P, P, P, I, I, I, I, P, P, P, I, I, P, P]
+    L.apex4_w4a4_linear_debug.argtypes = [P, P, P, I, I, I, I, P, P, P, I, I, P, ctypes.c_int, P]
+    L.apex4_tiled_weights_size.argtypes = [I, I, P]
+    L.apex4_tile_weights.argtypes = [P, I, I, P, P]
+    L.apex4_w4a4_gemm_tiled.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
+    L.apex4_w4a4_linear_tiled.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
     L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
     L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
     L.apex4_quantize_mx.argtypes = [P, I, I, I, P, P, P]
@@ -74,7 +80,8 @@ def lib() -> ctypes.CDLL:
               "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6",
               "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
               "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
-              "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws"):
+              "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws", "apex4_tiled_weights_size",
+              "apex4_tile_weights", "apex4_w4a4_gemm_tiled", "apex4_w4a4_linear_tiled"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -208,10 +215,11 @@ def apex4_w4a4_gemm_debug(A_q, s_a, W_q, s_w, G: int, m0: int = 0, mr: int | Non
                           flags: int = 0, Y=None, P=None, stream=None):
     """Y of apex4_w4a4_gemm (workspace None) or apex4_w4a4_gemm_ws (workspace a
     uint8 device tensor) and, from the same launches, the exact int32 group
-    sums P[i, n, g] of rows m0 .. m0+mr-1.  Returns (Y, P)."""
+    sums P[i, n, g] of rows m0 .. m0+mr-1.  Returns (Y, P).  With
+    flags & APEX4_DEBUG_W_TILED, W_q is tiled (N from s_w)."""
     import torch
     M, K2 = A_q.shape
-    N, K = W_q.shape[0], 2 * K2
+    N, K = s_w.shape[0], 2 * K2
     mr, P = _window(M, N, K, G, m0, mr, P, A_q.device)
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
@@ -254,12 +262,13 @@ def apex4_w4a4_gemm_plan(entry: str, M: int, N: int, K: int, G: int, flags: int 
 
 
 def apex4_w4a4_linear_debug(x, W_q, s_w, G: int, m0: int = 0, mr: int | None = None, Y=None, A_q_work=None,
-                            s_a_work=None, P=None, stream=None):
-    """apex4_w4a4_linear plus the exact int32 group sums of rows m0 .. m0+mr-1
-    from the same kernels.  Returns (Y, A_q_work, s_a_work, P)."""
+                            s_a_work=None, P=None, flags: int = 0, stream=None):
+    """apex4_w4a4_linear (or, with flags=APEX4_DEBUG_W_TILED, apex4_w4a4_linear_tiled)
+    plus the exact int32 group sums of rows m0 .. m0+mr-1 from the same
+    kernels.  Returns (Y, A_q_work, s_a_work, P)."""
     import torch
     M, K = x.shape
-    N = W_q.shape[0]
+    N = s_w.shape[0]
     mr, P = _window(M, N, K, G, m0, mr, P, x.device)
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float16, device=x.device)
@@ -270,9 +279,65 @@ def apex4_w4a4_linear_debug(x, W_q, s_w, G: int, m0: int = 0, mr: int | None = N
     rc = lib().apex4_w4a4_linear_debug(_dev(x, torch.float16, "x"), _dev(W_q, torch.uint8, "W_q"),
                                        _dev(s_w, torch.float16, "s_w"), M, N, K, G, _dev(Y, torch.float16, "Y"),
                                        _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
-                                       m0, mr, _dev(P, torch.int32, "P"), _stream(x, stream))
+                                       m0, mr, _dev(P, torch.int32, "P"), flags, _stream(x, stream))
     _check("apex4_w4a4_linear_debug", rc)
     return Y, A_q_work, s_a_work, P
+
+
+def apex4_tiled_weights_size(N: int, K: int) -> int:
+    """Bytes of the tiled layout of an [N, K/2] packed weight matrix."""
+    b = ctypes.c_int64(0)
+    _check("apex4_tiled_weights_size", lib().apex4_tiled_weights_size(N, K, ctypes.byref(b)))
+    return int(b.value)
+
+
+def apex4_tile_weights(W_q, W_t=None, stream=None):
+    """Packed weight codes uint8 [N, K/2] -> the tiled layout, a flat uint8 tensor
+    (offline, once per weight matrix)."""
+    import torch
+    N, K2 = W_q.shape
+    if W_t is None:
+        W_t = torch.empty((apex4_tiled_weights_size(N, 2 * K2),), dtype=torch.uint8, device=W_q.device)
+    rc = lib().apex4_tile_weights(_dev(W_q, torch.uint8, "W_q"), N, 2 * K2, _dev(W_t, torch.uint8, "W_t"),
+                                  _stream(W_q, stream))
+    _check("apex4_tile_weights", rc)
+    return W_t
+
+
+def apex4_w4a4_gemm_tiled(A_q, s_a, W_t, s_w, G: int, workspace=None, Y=None, stream=None):
+    """apex4_w4a4_gemm on tiled weights (N from s_w); with a workspace tensor, the
+    apex4_w4a4_gemm_ws kernel choice (split over K where it applies)."""
+    import torch
+    M, K2 = A_q.shape
+    N = s_w.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=A_q.device)
+    ws = ctypes.c_void_p(0) if workspace is None else _dev(workspace, torch.uint8, "workspace")
+    rc = lib().apex4_w4a4_gemm_tiled(_dev(A_q, torch.uint8, "A_q"), _dev(s_a, torch.float16, "s_a"),
+                                     _dev(W_t, torch.uint8, "W_t"), _dev(s_w, torch.float16, "s_w"), M, N, 2 * K2, G,
+                                     _dev(Y, torch.float16, "Y"), ws, 0 if workspace is None else workspace.numel(),
+                                     _stream(A_q, stream))
+    _check("apex4_w4a4_gemm_tiled", rc)
+    return Y
+
+
+def apex4_w4a4_linear_tiled(x, W_t, s_w, G: int, Y=None, A_q_work=None, s_a_work=None, stream=None):
+    """apex4_w4a4_linear on tiled weights (N from s_w)."""
+    import torch
+    M, K = x.shape
+    N = s_w.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    if A_q_work is None:
+        A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if s_a_work is None:
+        s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
+    rc = lib().apex4_w4a4_linear_tiled(_dev(x, torch.float16, "x"), _dev(W_t, torch.uint8, "W_t"),
+                                       _dev(s_w, torch.float16, "s_w"), M, N, K, G, _dev(Y, torch.float16, "Y"),
+                                       _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
+                                       _stream(x, stream))
+    _check("apex4_w4a4_linear_tiled", rc)
+    return Y
 
 
 def apex4_pack_fp6(q4, q6=None, stream=None):
@@ -361,58 +426,93 @@ def apex4_version() -> int:
 class W4A4Linear:
     """Drop-in W4A4 linear layer over the C ABI (APEX4 Sec. 3.2.1, Sec. 4.4):
     the fp16 weight [N, K] is quantized once with SymQuant (b=4, group G, the
-    same formula as the activations), and every forward quantizes the fp16
-    activations on the fly and runs the W4A4 GEMM (apex4_w4a4_linear).
+    same formula as the activations) and packed offline, and every forward
+    quantizes the fp16 activations on the fly and runs the W4A4 GEMM.
 
         lin = W4A4Linear(weight_fp16_cuda, G=128)
         y = lin(x)             # x [..., K] float16 on the same device -> [..., N]
+
+    layout="auto" keeps the weights in the tiled layout (apex4_tile_weights)
+    where it applies (G >= 128, fp16 scales) and row-major otherwise; "rows"
+    or "tiled" force one.  Only that copy is kept (W_q for rows, W_t for
+    tiled).
 
     scales="mx" selects the MX variant instead: power-of-two group scales
     applied inside the FP6 matrix instruction (apex4_quantize_mx +
     apex4_w4a4_gemm_mx_ws; G in 32..1024) -- not the paper's fp16 scales.
 
-    The work buffers for the quantized activations (and, for row counts whose
-    GEMM is split over K, its workspace) are kept and reused while the row
-    count stays the same.  Bias and other dtypes are not supported: the
-    paper's layers are bias-free fp16 linears."""
+    Work buffers (quantized activations, split-K workspace) are cached per
+    (row count, stream), so forwards on different streams never share them;
+    calls with the same row count on one stream reuse them in stream order.
+    Bias and other dtypes are not supported: the paper's layers are bias-free
+    fp16 linears."""
 
-    def __init__(self, weight, G: int = 128, scales: str = "fp16"):
+    MAX_CACHED = 8
+
+    def __init__(self, weight, G: int = 128, scales: str = "fp16", layout: str = "auto"):
         import torch
         if weight.dim() != 2:
             raise ValueError("weight must be [N, K]")
         if scales not in ("fp16", "mx"):
             raise ValueError("scales must be 'fp16' or 'mx'")
+        if layout not in ("auto", "rows", "tiled"):
+            raise ValueError("layout must be 'auto', 'rows' or 'tiled'")
         self.N, self.K = weight.shape
         self.G = self.K if G in (0, None) else int(G)
         self.mx = scales == "mx"
+        tiled_ok = not self.mx and self.G >= 128
+        if layout == "tiled" and not tiled_ok:
+            raise ValueError("the tiled layout needs fp16 scales and G >= 128")
+        self.tiled = tiled_ok if layout == "auto" else layout == "tiled"
         quant = apex4_quantize_mx if self.mx else apex4_quantize_act
-        self.W_q, self.s_w = quant(weight.contiguous(), self.G)
-        self._work = None
+        W_q, self.s_w = quant(weight.contiguous(), self.G)
+        self.W_q, self.W_t = (None, apex4_tile_weights(W_q)) if self.tiled else (W_q, None)
+        del W_q
+        self._work = {}
         self.device = weight.device
         self._torch = torch
 
-    def __call__(self, x):
-        lead = x.shape[:-1]
-        if x.shape[-1] != self.K:
-            raise ValueError(f"expected last dimension {self.K}, got {x.shape[-1]}")
-        x2 = x.reshape(-1, self.K).contiguous()
-        M = x2.shape[0]
-        if self._work is None or self._work[0].shape[0] != M:
+    def _buffers(self, M, stream):
+        key = (M, stream.cuda_stream)
+        buf = self._work.pop(key, None)
+        if buf is None:
             torch = self._torch
             size = apex4_w4a4_gemm_mx_workspace_size if self.mx else apex4_w4a4_gemm_workspace_size
             need = size(M, self.N, self.K, self.G) if M else 0
             codes = (M, 3 * self.K // 4) if self.mx else (M, self.K // 2)
             sdt = torch.uint8 if self.mx else torch.float16
-            self._work = (torch.empty(codes, dtype=torch.uint8, device=x2.device),
-                          torch.empty((M, max(self.K // self.G, 1)), dtype=sdt, device=x2.device),
-                          torch.empty((need,), dtype=torch.uint8, device=x2.device) if need else None)
-        Aq, sa, ws = self._work
+            buf = (torch.empty(codes, dtype=torch.uint8, device=self.device),
+                   torch.empty((M, max(self.K // self.G, 1)), dtype=sdt, device=self.device),
+                   torch.empty((need,), dtype=torch.uint8, device=self.device) if need else None)
+            while len(self._work) >= self.MAX_CACHED:
+                self._work.pop(next(iter(self._work)))
+        self._work[key] = buf  # most recently used last
+        return buf
+
+    def __call__(self, x, stream=None):
+        lead = x.shape[:-1]
+        if x.shape[-1] != self.K:
+            raise ValueError(f"expected last dimension {self.K}, got {x.shape[-1]}")
+        x2 = x.reshape(-1, self.K).contiguous()
+        M = x2.shape[0]
+        if stream is None:
+            stream = self._torch.cuda.current_stream(x2.device)
+        Aq, sa, ws = self._buffers(M, stream)
         if self.mx:
-            apex4_quantize_mx(x2, self.G, Aq, sa)
-            Y = apex4_w4a4_gemm_mx_ws(Aq, sa, self.W_q, self.s_w, self.G, ws)
+            apex4_quantize_mx(x2, self.G, Aq, sa, stream=stream)
+            if ws is None:
+                Y = apex4_w4a4_gemm_mx(Aq, sa, self.W_q, self.s_w, self.G, stream=stream)
+            else:
+                Y = apex4_w4a4_gemm_mx_ws(Aq, sa, self.W_q, self.s_w, self.G, ws, stream=stream)
+        elif self.tiled:
+            if ws is None:
+                Y = apex4_w4a4_linear_tiled(x2, self.W_t, self.s_w, self.G, None, Aq, sa, stream=stream)
+            else:
+                apex4_quantize_act(x2, self.G, Aq, sa, stream=stream)
+                Y = apex4_w4a4_gemm_tiled(Aq, sa, self.W_t, self.s_w, self.G, ws, stream=stream)
         elif ws is None:
-            Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, Aq, sa)
+            Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, Aq, sa, stream=stream)
         else:
-            apex4_quantize_act(x2, self.G, Aq, sa)
-            Y = apex4_w4a4_gemm_ws(Aq, sa, self.W_q, self.s_w, self.G, ws)
+            apex4_quantize_act(x2, self.G, Aq, sa, stream=stream)
+            Y = apex4_w4a4_gemm_ws(Aq, sa, self.W_q, self.s_w, self.G, ws, stream=stream)
         return Y.reshape(*lead, self.N)

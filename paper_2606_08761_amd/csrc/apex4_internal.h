@@ -19,7 +19,14 @@ struct Dump {
 };
 
 // K stages of 128 codes covering K (the last one partial when K % 128 != 0).
-inline int64_t kstages(int64_t K) { return (K + 127) / 128; }
+__host__ __device__ inline int64_t kstages(int64_t K) { return (K + 127) / 128; }
+
+// Tiled weight layout (wt): [ceil(N/32)][kstages(K)][2][64][16 B], zero padded.
+// Piece (t, s, j, l) holds bytes [64 s + 32 (l / 32) + 16 j, + 16) of the packed
+// row 32 t + l % 32: the 32 bytes lane l of a 32-column MFMA fragment consumes
+// in stage s are contiguous, and a wave's fragment is one 2 KB block.
+inline int64_t tiled_weight_bytes(int64_t N, int64_t K) { return ((N + 31) / 32) * kstages(K) * 2048; }
+hipError_t launch_tile_weights(const uint8_t* Wq, int64_t N, int64_t K, uint8_t* Wt, hipStream_t stream);
 
 // Activation/weight quantizer (SymQuant, b = 4).
 hipError_t launch_quantize(const uint16_t* x, int64_t M, int64_t K, int64_t G,
@@ -48,7 +55,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool 
 // window's group sums; sa == sw == nullptr then skips the scales and Y.
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                        const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
-                       uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool force_tile = false);
+                       uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool force_tile = false,
+                       bool wt = false);
 
 // int32 fill of n elements (dump buffers that receive atomic partial sums).
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream);
@@ -62,7 +70,7 @@ int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G);
 int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
-                              hipStream_t stream, Dump dump = Dump(), bool force_tile = false);
+                              hipStream_t stream, Dump dump = Dump(), bool force_tile = false, bool wt = false);
 
 // Y = binary16(sum of the S fp32 planes part[S][M N]) in plane order.
 hipError_t launch_splitk_reduce(const float* part, int S, int64_t MN, uint16_t* Y, hipStream_t stream);
@@ -75,23 +83,24 @@ int device_cu_count();
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                               const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
-                              uint16_t* Y, hipStream_t stream, Dump dump = Dump());
+                              uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool wt = false);
 
 // W4A4 GEMM for one row on the vector ALUs (v_dot8_i32_i4 on the packed
 // codes): weight rows streamed from HBM in 1 KB runs.  gemv_fits() says
 // whether the shape is one it handles.
 bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump = Dump());
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump = Dump(),
+                       bool wt = false);
 
 // Quantize + W4A4 GEMM in one kernel: the one-row kernel above, quantizing x
 // in its prologue (G in {32, 64, 128, 256, 512}, G < K).  Y as
 // launch_quantize followed by launch_gemm gives, bit for bit, and Aq / sa
 // receive the same codes and scales as launch_quantize writes.
-bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G);
+bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G, bool wt = false);
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N,
                                int64_t K, int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream,
-                               Dump dump = Dump());
+                               Dump dump = Dump(), bool wt = false);
 
 // The 4-bit codes in FP6 e3m2 containers (6-bit fields, little-endian, 3K/4
 // bytes per row) and the G = 128 GEMM on the FP6 matrix cores that reads them.

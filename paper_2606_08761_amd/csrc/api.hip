@@ -143,7 +143,7 @@ namespace {
 // with an optional dump of exact group sums and the general-tile switch.
 int gemm_dispatch(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N,
                   int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes, apex4::Dump dump,
-                  bool general, void* stream) {
+                  bool general, bool wt, void* stream) {
     const auto sa = static_cast<const uint16_t*>(s_a);
     const auto sw = static_cast<const uint16_t*>(s_w);
     const auto y = static_cast<uint16_t*>(Y);
@@ -151,13 +151,21 @@ int gemm_dispatch(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const
     const int64_t need = workspace ? apex4::splitk_workspace_bytes(M, N, K, G) : 0;
     hipError_t e;
     if (need == 0) {
-        e = apex4::launch_gemm(A_q, sa, W_q, sw, M, N, K, G, y, st, dump, general);
+        e = apex4::launch_gemm(A_q, sa, W_q, sw, M, N, K, G, y, st, dump, general, wt);
     } else {
         if (workspace_bytes < need) return APEX4_ERR_WORKSPACE;
         e = apex4::launch_gemm_splitk(A_q, sa, W_q, sw, M, N, K, G, y, static_cast<float*>(workspace), st, dump,
-                                      general);
+                                      general, wt);
     }
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+// Tiled weights (apex4_tile_weights): one group per 128-wide stage or more, and
+// 32-bit offsets into the tiled buffer.
+int check_tiled(int64_t N, int64_t K, int64_t G) {
+    if (G < 128) return APEX4_ERR_GROUP;
+    if (apex4::tiled_weight_bytes(N, K) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
+    return APEX4_OK;
 }
 
 int check_window(int64_t M, int64_t m0, int64_t mr, const void* P) {
@@ -179,7 +187,8 @@ int apex4_w4a4_gemm_ws(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, 
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
     if (!workspace && apex4::splitk_workspace_bytes(M, N, K, G) > 0) return APEX4_ERR_WORKSPACE;
-    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, workspace, workspace_bytes, apex4::Dump(), false, stream);
+    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, workspace, workspace_bytes, apex4::Dump(), false, false,
+                         stream);
 }
 
 int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M, int64_t N, int64_t K,
@@ -198,7 +207,7 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M,
     // the full M x N problem through apex4_w4a4_gemm's kernel choice, without
     // scales (no Y): only the window's sums are written
     const apex4::Dump dump{P, static_cast<int>(m0), static_cast<int>(mr)};
-    return gemm_dispatch(A_q, nullptr, W_q, nullptr, M, N, K, G, nullptr, nullptr, 0, dump, false, stream);
+    return gemm_dispatch(A_q, nullptr, W_q, nullptr, M, N, K, G, nullptr, nullptr, 0, dump, false, false, stream);
 }
 
 }  // extern "C"
@@ -248,7 +257,7 @@ int apex4_w4a4_gemm_noalloc(const uint8_t* A_q, const void* s_a, const uint8_t* 
     }
     // every partial plane element is written before the reduce reads it: the
     // scratch needs no clearing
-    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, ws, need, apex4::Dump(), false, stream);
+    return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, ws, need, apex4::Dump(), false, false, stream);
 }
 
 int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a, const uint8_t* W_q, const void* s_w, int64_t M,
@@ -258,7 +267,9 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a, const uint8_t* W_
     int rc = check_gemm_args(A_q, s_a, W_q, s_w, M, N, K, G, Y);
     if (rc) return rc;
     if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
-    if (flags & ~APEX4_DEBUG_GENERAL_TILES) return APEX4_ERR_SHAPE;
+    if (flags & ~(APEX4_DEBUG_GENERAL_TILES | APEX4_DEBUG_W_TILED)) return APEX4_ERR_SHAPE;
+    const bool wt = (flags & APEX4_DEBUG_W_TILED) != 0;
+    if (wt && (rc = check_tiled(N, K, G))) return rc;
     rc = check_window(M, m0, mr, P);
     if (rc) return rc;
     rc = check_device();
@@ -266,25 +277,57 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a, const uint8_t* W_
     if (M == 0) return APEX4_OK;
     const apex4::Dump dump{mr > 0 ? P : nullptr, static_cast<int>(m0), static_cast<int>(mr)};
     return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, workspace, workspace_bytes, dump,
-                         (flags & APEX4_DEBUG_GENERAL_TILES) != 0, stream);
+                         (flags & APEX4_DEBUG_GENERAL_TILES) != 0, wt, stream);
+}
+
+int apex4_tiled_weights_size(int64_t N, int64_t K, int64_t* bytes) {
+    if (!bytes) return APEX4_ERR_NULL;
+    if (N < 1 || K < 32 || (K % 32) != 0 || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    *bytes = apex4::tiled_weight_bytes(N, K);
+    return APEX4_OK;
+}
+
+int apex4_tile_weights(const uint8_t* W_q, int64_t N, int64_t K, uint8_t* W_t, void* stream) {
+    if (!W_q || !W_t) return APEX4_ERR_NULL;
+    if (N < 1 || K < 32 || (K % 32) != 0 || N > 0x7FFFFFFF || K > 0x7FFFFFFF) return APEX4_ERR_SHAPE;
+    if (N * (K / 2) > 0xFFFFFFFFll || apex4::tiled_weight_bytes(N, K) > 0xFFFFFFFFll) return APEX4_ERR_SHAPE;
+    if (!aligned16(W_q) || !aligned16(W_t)) return APEX4_ERR_ALIGN;
+    const int rc = check_device();
+    if (rc) return rc;
+    const hipError_t e = apex4::launch_tile_weights(W_q, N, K, W_t, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
+}
+
+int apex4_w4a4_gemm_tiled(const uint8_t* A_q, const void* s_a, const uint8_t* W_t, const void* s_w, int64_t M,
+                          int64_t N, int64_t K, int64_t G, void* Y, void* workspace, int64_t workspace_bytes,
+                          void* stream) {
+    int rc = check_gemm_args(A_q, s_a, W_t, s_w, M, N, K, G, Y);
+    if (rc) return rc;
+    if ((rc = check_tiled(N, K, G))) return rc;
+    if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    return gemm_dispatch(A_q, s_a, W_t, s_w, M, N, K, G, Y, workspace, workspace_bytes, apex4::Dump(), false, true,
+                         stream);
 }
 
 namespace {
 
 int linear_dispatch(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K, int64_t G,
-                    void* Y, uint8_t* A_q_work, void* s_a_work, apex4::Dump dump, void* stream) {
+                    void* Y, uint8_t* A_q_work, void* s_a_work, apex4::Dump dump, bool wt, void* stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     const auto xh = static_cast<const uint16_t*>(x);
     const auto sw = static_cast<const uint16_t*>(s_w);
     const auto sa = static_cast<uint16_t*>(s_a_work);
     const auto y = static_cast<uint16_t*>(Y);
-    if (apex4::fused_linear_fits(M, N, K, G)) {
-        const hipError_t e = apex4::launch_linear_fused(xh, W_q, sw, M, N, K, G, y, A_q_work, sa, st, dump);
+    if (apex4::fused_linear_fits(M, N, K, G, wt)) {
+        const hipError_t e = apex4::launch_linear_fused(xh, W_q, sw, M, N, K, G, y, A_q_work, sa, st, dump, wt);
         return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
     }
     hipError_t e = apex4::launch_quantize(xh, M, K, G, A_q_work, sa, st);
     if (e != hipSuccess) return APEX4_ERR_LAUNCH;
-    e = apex4::launch_gemm(A_q_work, sa, W_q, sw, M, N, K, G, y, st, dump);
+    e = apex4::launch_gemm(A_q_work, sa, W_q, sw, M, N, K, G, y, st, dump, false, wt);
     return e == hipSuccess ? APEX4_OK : APEX4_ERR_LAUNCH;
 }
 
@@ -306,22 +349,36 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w, int64_
     rc = check_device();
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
-    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), stream);
+    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), false, stream);
+}
+
+int apex4_w4a4_linear_tiled(const void* x, const uint8_t* W_t, const void* s_w, int64_t M, int64_t N, int64_t K,
+                            int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, void* stream) {
+    int rc = check_linear_args(x, W_t, s_w, M, N, K, G, Y, A_q_work, s_a_work);
+    if (rc) return rc;
+    if ((rc = check_tiled(N, K, G))) return rc;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    return linear_dispatch(x, W_t, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), true, stream);
 }
 
 int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
                             int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, int64_t m0, int64_t mr, int32_t* P,
-                            void* stream) {
+                            int flags, void* stream) {
     if (!present(P, mr)) return APEX4_ERR_NULL;
     int rc = check_linear_args(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work);
     if (rc) return rc;
+    if (flags & ~APEX4_DEBUG_W_TILED) return APEX4_ERR_SHAPE;
+    const bool wt = flags != 0;
+    if (wt && (rc = check_tiled(N, K, G))) return rc;
     rc = check_window(M, m0, mr, P);
     if (rc) return rc;
     rc = check_device();
     if (rc) return rc;
     if (M == 0) return APEX4_OK;
     const apex4::Dump dump{mr > 0 ? P : nullptr, static_cast<int>(m0), static_cast<int>(mr)};
-    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, dump, stream);
+    return linear_dispatch(x, W_q, s_w, M, N, K, G, Y, A_q_work, s_a_work, dump, wt, stream);
 }
 
 int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, int flags, int* kernel,
@@ -332,8 +389,10 @@ int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, 
     rc = check_gemm_group(K, G);
     if (rc) return rc;
     if (entry < APEX4_ENTRY_GEMM || entry > APEX4_ENTRY_LINEAR) return APEX4_ERR_SHAPE;
-    if (flags & ~APEX4_DEBUG_GENERAL_TILES) return APEX4_ERR_SHAPE;
-    if (entry == APEX4_ENTRY_LINEAR && flags) return APEX4_ERR_SHAPE;
+    if (flags & ~(APEX4_DEBUG_GENERAL_TILES | APEX4_DEBUG_W_TILED)) return APEX4_ERR_SHAPE;
+    if (entry == APEX4_ENTRY_LINEAR && (flags & APEX4_DEBUG_GENERAL_TILES)) return APEX4_ERR_SHAPE;
+    const bool wt = (flags & APEX4_DEBUG_W_TILED) != 0;
+    if (wt && (rc = check_tiled(N, K, G))) return rc;
     rc = check_device();
     if (rc) return rc;
     if (M == 0) {
@@ -341,7 +400,7 @@ int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, 
         *splits = 0;
         return APEX4_OK;
     }
-    if (entry == APEX4_ENTRY_LINEAR && apex4::fused_linear_fits(M, N, K, G)) {
+    if (entry == APEX4_ENTRY_LINEAR && apex4::fused_linear_fits(M, N, K, G, wt)) {
         *kernel = apex4::kKernelFused;
         *splits = 1;
         return APEX4_OK;

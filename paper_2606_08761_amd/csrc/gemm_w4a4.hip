@@ -60,6 +60,11 @@
 //   * K % 128 != 0 (K % 32 == 0; G in {32, 64} or G == K): the last stage is
 //     partial.  Its loads are masked to the row's end (lanes past it hold
 //     zero codes, which add nothing) and its missing groups are skipped.
+//   * Tiled weights (wt): W may come in the offline tiled layout, 32-row tiles
+//     by 128-wide K stages with each lane's 32 bytes of a stage stored
+//     contiguously ([N/32][K/128][2][64 lanes][16 B], zero padded), so that a
+//     wave's weight fragment for a stage is one contiguous 2 KB block.  Only
+//     the weight addressing changes (per-lane base, stage and half strides).
 //   * Dump (tests and diagnostics): the same kernels, instantiated with DUMP,
 //     also write the exact group sums of a row window, taken from the int32
 //     MFMA results before dequantization; the kernel choice (plan_gemm) is the
@@ -143,7 +148,7 @@ template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
-    int32_t* __restrict__ P, int pm0, int pmr, int nks_split, void* __restrict__ part) {
+    int32_t* __restrict__ P, int pm0, int pmr, int nks_split, void* __restrict__ part, int wt) {
     constexpr int NT = 64 * WAVES_M * WAVES_N;
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     constexpr int A_CH = BM * 4 / NT;                 // 16-byte packed activation chunks per thread
@@ -229,11 +234,22 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         sc_base = is_a ? sa : sw;
         sc_off = static_cast<uint32_t>(row) * static_cast<uint32_t>(ng);
     }
+    // weight bytes: row-major, lane base n K/2 + 32 h, stage stride 64, halves 16
+    // apart; tiled (G >= 128 only), lane base (tile stages) 2 KB + 16 lane, stage
+    // stride 2 KB, halves 1 KB apart
+    const bool tiled = !FINE && wt != 0;  // uniform
+    const int w_sstride = tiled ? 2048 : KS / 2;
+    const int w_jstride = tiled ? 1024 : 16;
     uint32_t w_off[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-        const int n = min(n0 + wn * NJ * 32 + j * 32 + l32, N - 1);
-        w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + (FINE ? 8 : 32) * lh;
+        if (tiled) {
+            const int t = min((n0 + wn * NJ * 32 + j * 32) / 32, (N + 31) / 32 - 1);
+            w_off[j] = static_cast<uint32_t>(t) * static_cast<uint32_t>(kstages(K)) * 2048u + 16u * lane;
+        } else {
+            const int n = min(n0 + wn * NJ * 32 + j * 32 + l32, N - 1);
+            w_off[j] = static_cast<uint32_t>(n) * static_cast<uint32_t>(K / 2) + (FINE ? 8 : 32) * lh;
+        }
     }
 
     // Global loads run PF stages ahead: stage s lives in register slot s % PF
@@ -294,9 +310,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     uint4 w[PF][NJ][2];
     auto load_w = [&](int ks, auto SLOT) __attribute__((always_inline)) {
         constexpr int sl = decltype(SLOT)::value;
-        const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2);
+        const uint8_t* base = Wq + static_cast<int64_t>(ks) * w_sstride;
         const int lim = kb - ks * (KS / 2);  // uniform
-        const bool full = lim >= KS / 2;
+        const bool full = tiled || lim >= KS / 2;  // the tiled layout is zero padded
         const uint2 z2 = make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -313,7 +329,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
             } else {
                 const int h32 = 32 * lh;
                 w[sl][j][0] = (full || h32 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j]) : make_uint4(0u, 0u, 0u, 0u);
-                w[sl][j][1] = (full || h32 + 16 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j] + 16)
+                w[sl][j][1] = (full || h32 + 16 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j] + w_jstride)
                                                        : make_uint4(0u, 0u, 0u, 0u);
             }
         }
@@ -681,7 +697,7 @@ template <bool DUMP>
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y, int nks_split,
-    float* __restrict__ part, int32_t* __restrict__ P, int pm0, int pmr) {
+    float* __restrict__ part, int32_t* __restrict__ P, int pm0, int pmr, int wt) {
     constexpr int NT = 512, BM = 128, BN = 256, MI = 4;
     __shared__ Stage<BM, NT, 1> st[2];
     const bool have_sc = !DUMP || sa != nullptr;  // uniform
@@ -724,7 +740,11 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const int srow = is_a ? min(m0 + tid, M - 1) : min(n0 + min(tid - BM, BN - 1), N - 1);
     const uint16_t* sc_base = is_a ? sa : sw;
     const uint32_t sc_off = static_cast<uint32_t>(srow) * static_cast<uint32_t>(ng);
-    const uint32_t w_off = static_cast<uint32_t>(min(n0 + wave * 32 + l32, N - 1)) * static_cast<uint32_t>(K / 2) + 32 * lh;
+    // weights: row-major or tiled, as in the kernel above
+    const uint32_t w_off =
+        wt ? static_cast<uint32_t>(min(nt * 8 + wave, (N + 31) / 32 - 1)) * static_cast<uint32_t>(K / KS) * 2048u + 16u * lane
+           : static_cast<uint32_t>(min(n0 + wave * 32 + l32, N - 1)) * static_cast<uint32_t>(K / 2) + 32 * lh;
+    const int w_sstride = wt ? 2048 : KS / 2, w_jstride = wt ? 1024 : 16;
 
     uint4 ra;
     uint16_t rsc;
@@ -741,9 +761,9 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     };
     auto load_w = [&](int ks) __attribute__((always_inline)) {
         ks = min(ks, nks - 1) + kofs;
-        const uint8_t* base = Wq + static_cast<int64_t>(ks) * (KS / 2) + w_off;
+        const uint8_t* base = Wq + static_cast<int64_t>(ks) * w_sstride + w_off;
         w[0] = *reinterpret_cast<const uint4*>(base);
-        w[1] = *reinterpret_cast<const uint4*>(base + 16);
+        w[1] = *reinterpret_cast<const uint4*>(base + w_jstride);
     };
 
     f32x16 acc[MI];
@@ -922,7 +942,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
 
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int KSPLIT, bool DUMP>
 hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                    int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
+                    int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
                     void* part = nullptr) {
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
@@ -935,7 +955,8 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
     hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT, DUMP>),
                        dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(64 * WAVES_M * WAVES_N * KSPLIT),
                        0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
-                       static_cast<int>(G), Y, dump.P, dump.m0, dump.mr, static_cast<int>(kstages(K) / S), part);
+                       static_cast<int>(G), Y, dump.P, dump.m0, dump.mr, static_cast<int>(kstages(K) / S), part,
+                       wt ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -947,54 +968,51 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
 // fit twice, and the split loses (N = 10240: 9 % slower).
 template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS = 1>
 hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                  int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
+                  int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
                   void* part = nullptr) {
     constexpr bool small = WAVES_M * WAVES_N * MI * NJ <= 8;
-    if (dump.P) {
-        if (S > 1)
-            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
-                                                                                    stream, S, part);
-        if constexpr (small) {
-            constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
-            const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-            const int64_t stages = kstages(K);
-            const int64_t spg = (MODE == kChannel || GPS > 1) ? 1 : G / KS;
-            if (tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0)
-                return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, true>(Aq, sa, Wq, sw, M, N, K, G, Y,
-                                                                                        dump, stream);
-        }
-        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
-                                                                                stream);
-    }
-    if (S > 1)  // split across workgroups: one wave group per workgroup
-        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
-                                                                                 stream, S, part);
+    int ksplit = 1;
     if constexpr (small) {
         constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
         const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
         const int64_t stages = kstages(K);
         const int64_t spg = (MODE == kChannel || GPS > 1) ? 1 : G / KS;
-        if (tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0)
-            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
-                                                                                     stream);
+        if (S == 1 && tiles <= device_cu_count() && stages % 2 == 0 && (stages / 2) % spg == 0) ksplit = 2;
     }
-    return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream);
+    // S > 1: split across workgroups, one wave group per workgroup
+    if (dump.P) {
+        if constexpr (small) {
+            if (ksplit == 2)
+                return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, true>(Aq, sa, Wq, sw, M, N, K, G, Y,
+                                                                                        dump, wt, stream);
+        }
+        return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt,
+                                                                                stream, S, part);
+    }
+    if constexpr (small) {
+        if (ksplit == 2)
+            return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 2, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump,
+                                                                                     wt, stream);
+    }
+    return launch_k<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, 1, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt,
+                                                                             stream, S, part);
 }
 
 // The G = 128 ping-pong kernel on 128 x 256 tiles (S > 1: split over K, fp32
 // partial tiles to part).
 hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                     int64_t N, int64_t K, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1, float* part = nullptr) {
+                     int64_t N, int64_t K, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
+                     float* part = nullptr) {
     const int64_t tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(tiles), static_cast<unsigned>(S));
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), nks = static_cast<int>(K / KS / S);
     if (dump.P)
         hipLaunchKernelGGL(w4a4_gemm_pp_kernel<true>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
-                           dump.P, dump.m0, dump.mr);
+                           dump.P, dump.m0, dump.mr, wt ? 1 : 0);
     else
         hipLaunchKernelGGL(w4a4_gemm_pp_kernel<false>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
-                           static_cast<int32_t*>(nullptr), 0, 0);
+                           static_cast<int32_t*>(nullptr), 0, 0, wt ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -1007,19 +1025,20 @@ hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, c
 // force_general.
 template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                        int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, hipStream_t stream, int S = 1,
+                        int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
                         void* part = nullptr, bool force_general = false) {
-    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
-    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
-    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+    if (G == K) return launch<1, WAVES_N, MI, 1, kChannel, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
+    if (G == 32) return launch<1, WAVES_N, MI, 1, kRotate, true, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
+    if (G == 64) return launch<1, WAVES_N, MI, 1, kRotate, true, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
     if (G == 128) {
         if constexpr (WAVES_N == 8 && MI == 4) {
-            if (!force_general) return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, stream, S, static_cast<float*>(part));
+            if (!force_general)
+                return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, S, static_cast<float*>(part));
         }
-        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+        return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
     }
-    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
-    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, S, part);
+    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
+    return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
 }
 
 namespace {
@@ -1154,14 +1173,15 @@ namespace {
 
 hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                           const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y,
-                          hipStream_t stream, Dump dump, float* part) {
+                          hipStream_t stream, Dump dump, float* part, bool wt) {
     switch (plan.kernel) {
-        case kKernelGemv: return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump);
-        case kKernelDecode: return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump);
-        case kKernelTile64: return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, plan.splits, part);
+        case kKernelGemv: return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, wt);
+        case kKernelDecode: return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, wt);
+        case kKernelTile64:
+            return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, plan.splits, part);
         case kKernelTile128:
-            return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, stream, 1, nullptr, /*force_general=*/true);
-        case kKernelPingPong: return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, stream, plan.splits, part);
+            return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, 1, nullptr, /*force_general=*/true);
+        case kKernelPingPong: return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, plan.splits, part);
         default: return hipErrorInvalidValue;
     }
 }
@@ -1170,15 +1190,15 @@ hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_
 
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
-                              hipStream_t stream, Dump dump, bool force_tile) {
+                              hipStream_t stream, Dump dump, bool force_tile, bool wt) {
     const GemmPlan plan = plan_gemm(M, N, K, G, true, force_tile);
-    if (plan.splits < 2) return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, nullptr);
+    if (plan.splits < 2) return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, nullptr, wt);
     const int S = plan.splits;
     // split ranges hold whole groups, so every group sum except the
     // per-channel one is dumped by the kernel that completes it
     Dump tile_dump = dump;
     if (G == K) tile_dump.P = nullptr;
-    const hipError_t e = launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, tile_dump, part);
+    const hipError_t e = launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, tile_dump, part, wt);
     if (e != hipSuccess) return e;
     if (G == K) {
         const int64_t need = (M * N + 255) / 256;
@@ -1195,9 +1215,9 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
 // otherwise the tile kernels (the same choice with or without a dump).
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump,
-                       bool force_tile) {
+                       bool force_tile, bool wt) {
     return launch_planned(plan_gemm(M, N, K, G, false, force_tile), Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump,
-                          nullptr);
+                          nullptr, wt);
 }
 
 }  // namespace apex4

@@ -27,6 +27,11 @@
 //     instead of its codes and quantizes it into LDS in the prologue with the
 //     quantizer's own arithmetic (quant_core.h: same codes and scales, bit for
 //     bit); workgroup 0 also writes them to the caller's work buffers.
+//   * Tiled weights (w4a4_gemv_tiled_kernel): W in the tiled layout
+//     (apex4_internal.h), where a 1 KB run holds 16 bytes of each of 32 rows:
+//     a workgroup takes one 32-row tile and its 8 waves split the tile's 1 KB
+//     runs; lanes l and l + 32 hold the same row, so a row's sum is one
+//     shuffle, then the waves' partials are added in a fixed order in LDS.
 //   * DUMP (pmr == 1): every lane's exact 32-code partial sum is added with an
 //     integer atomic into the zeroed P[1][N][K/G], giving the exact group sums
 //     whatever the order; sa == nullptr (codes only) skips the scales and Y.
@@ -53,6 +58,66 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) v += __shfl_xor(v, d, 64);
     return v;
+}
+
+// A's codes (K/2 bytes) into gv_lds and s_a as binary32 [K/G] into sa_lds, by
+// the NT threads of a workgroup: copied from Aq / sa, or (FUSE) quantized from
+// the binary16 row x with the quantizer's arithmetic (quant_core.h: the same
+// codes and scales, bit for bit), which workgroup 0 also writes to aq_out /
+// sa_out.  QL = G / 8: slots of 8 values per group (FUSE only).
+template <bool FUSE, int QL, int NT>
+__device__ __forceinline__ void gv_stage_a(uint4* gv_lds, float* sa_lds, const uint8_t* __restrict__ Aq,
+                                           const uint16_t* __restrict__ sa, bool have_sc, int K, int ng,
+                                           const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out,
+                                           uint16_t* __restrict__ sa_out) {
+    const int tid = threadIdx.x;
+    [[maybe_unused]] const int kb = K / 2;
+    if constexpr (FUSE) {
+        // SymQuant of x in slots of 8 values (slot s: k in [8 s, 8 s + 8)),
+        // QL consecutive slots per group.  Slot base + tid + u NT is
+        // lane-consecutive, so a group is QL neighbouring lanes of one wave,
+        // all active (slots past K load zeros: code 0, scale 0).
+        const int nslots = K / 8;
+        uint4 v[GV_FQ];
+        auto load_x = [&](int base) __attribute__((always_inline)) {
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                const int s = base + tid + u * NT;
+                v[u] = s < nslots ? *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(s) * 8) : make_uint4(0u, 0u, 0u, 0u);
+            }
+        };
+        load_x(0);
+        for (int base = 0; base < nslots; base += GV_FQ * NT) {
+            uint32_t packed[GV_FQ];
+            uint16_t sbits[GV_FQ];
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                if (base + u * NT < nslots) {  // uniform: thread 0 has a slot
+                    const uint32_t am = quant::group_max<QL>(quant::absmax8_bits(v[u]));
+                    const float sf = quant::scale_of(am, &sbits[u]);
+                    packed[u] = quant::pack8(v[u], sf, quant::inv_of(sf));
+                }
+            }
+            if (base + GV_FQ * NT < nslots) load_x(base + GV_FQ * NT);
+#pragma unroll
+            for (int u = 0; u < GV_FQ; ++u) {
+                const int s = base + tid + u * NT;
+                if (s < nslots) {
+                    reinterpret_cast<uint32_t*>(gv_lds)[s] = packed[u];
+                    const bool lead = (s & (QL - 1)) == 0;
+                    if (lead) sa_lds[s / QL] = gv_h2f(sbits[u]);
+                    if (blockIdx.x == 0) {
+                        reinterpret_cast<uint32_t*>(aq_out)[s] = packed[u];
+                        if (lead) sa_out[s / QL] = sbits[u];
+                    }
+                }
+            }
+        }
+    } else {
+        for (int i = tid; i < kb / 16; i += NT) gv_lds[i] = reinterpret_cast<const uint4*>(Aq)[i];
+        if (have_sc)
+            for (int i = tid; i < ng; i += NT) sa_lds[i] = gv_h2f(sa[i]);
+    }
 }
 
 // Wave w of workgroup b owns weight rows n0 .. n0 + rpw - 1,
@@ -99,52 +164,7 @@ __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
 
     if (n0 < N) issue(0);
     // A's codes and scales into LDS while the first weight loads are in flight
-    if constexpr (FUSE) {
-        // SymQuant of x in slots of 8 values (slot s: k in [8 s, 8 s + 8)),
-        // QL consecutive slots per group.  Slot base + tid + u GV_NT is
-        // lane-consecutive, so a group is QL neighbouring lanes of one wave,
-        // all active (slots past K load zeros: code 0, scale 0).
-        const int nslots = K / 8;
-        uint4 v[GV_FQ];
-        auto load_x = [&](int base) __attribute__((always_inline)) {
-#pragma unroll
-            for (int u = 0; u < GV_FQ; ++u) {
-                const int s = base + tid + u * GV_NT;
-                v[u] = s < nslots ? *reinterpret_cast<const uint4*>(x + static_cast<int64_t>(s) * 8) : make_uint4(0u, 0u, 0u, 0u);
-            }
-        };
-        load_x(0);
-        for (int base = 0; base < nslots; base += GV_FQ * GV_NT) {
-            uint32_t packed[GV_FQ];
-            uint16_t sbits[GV_FQ];
-#pragma unroll
-            for (int u = 0; u < GV_FQ; ++u) {
-                if (base + u * GV_NT < nslots) {  // uniform: thread 0 has a slot
-                    const uint32_t am = quant::group_max<QL>(quant::absmax8_bits(v[u]));
-                    const float sf = quant::scale_of(am, &sbits[u]);
-                    packed[u] = quant::pack8(v[u], sf, quant::inv_of(sf));
-                }
-            }
-            if (base + GV_FQ * GV_NT < nslots) load_x(base + GV_FQ * GV_NT);
-#pragma unroll
-            for (int u = 0; u < GV_FQ; ++u) {
-                const int s = base + tid + u * GV_NT;
-                if (s < nslots) {
-                    reinterpret_cast<uint32_t*>(gv_lds)[s] = packed[u];
-                    const bool lead = (s & (QL - 1)) == 0;
-                    if (lead) sa_lds[s / QL] = gv_h2f(sbits[u]);
-                    if (blockIdx.x == 0) {
-                        reinterpret_cast<uint32_t*>(aq_out)[s] = packed[u];
-                        if (lead) sa_out[s / QL] = sbits[u];
-                    }
-                }
-            }
-        }
-    } else {
-        for (int i = tid; i < kb / 16; i += GV_NT) gv_lds[i] = reinterpret_cast<const uint4*>(Aq)[i];
-        if (have_sc)
-            for (int i = tid; i < ng; i += GV_NT) sa_lds[i] = gv_h2f(sa[i]);
-    }
+    gv_stage_a<FUSE, QL, GV_NT>(gv_lds, sa_lds, Aq, sa, have_sc, K, ng, x, aq_out, sa_out);
     __syncthreads();
     if (n0 >= N) return;  // after the only barrier
 
@@ -186,7 +206,114 @@ __global__ __launch_bounds__(GV_NT) void w4a4_gemv_kernel(
     }
 }
 
+constexpr int GT_WAVES = 8;  // tiled: waves per workgroup (one 32-row tile)
+constexpr int GT_NT = 64 * GT_WAVES;
+constexpr int GT_MAX_LDS = 128 * 1024 + 1024;  // dynamic LDS of the tiled kernel (the static part is 1 KB)
+constexpr int GT_SWP = 16;                      // weight scales per thread loaded ahead (K/G <= 256 in full)
+
+// One row against tiled weights.  Workgroup t owns rows 32 t .. 32 t + 31; its
+// wave w takes the tile's 1 KB runs q = w, w + GT_WAVES, ... (run q = stage
+// q / 2, half q % 2), GV_LOADS at a time; lane l holds row 32 t + l % 32 and the
+// 32 codes at packed bytes 64 (q / 2) + 32 (l / 32) + 16 (q % 2).  G >= 128, so
+// a run lies in one group, g = 128 (q / 2) / G for every lane: the tile's
+// weight scales are staged in LDS group-major ([K/G][32], one coalesced pass)
+// and a run reads 32 consecutive ones.
+template <bool FUSE, int QL, bool DUMP>
+__global__ __launch_bounds__(GT_NT) void w4a4_gemv_tiled_kernel(
+    const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wt,
+    const uint16_t* __restrict__ sw, int N, int K, int G, int lgG, uint16_t* __restrict__ Y,
+    const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out,
+    int32_t* __restrict__ P, int pmr) {
+    const bool have_sc = FUSE || !DUMP || sa != nullptr;  // uniform
+    extern __shared__ uint4 gv_lds[];
+    __shared__ float red[GT_WAVES][32];
+    const int tid = threadIdx.x, lane = tid & 63, lh = lane >> 5;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kb = K / 2;
+    const int ng = K / G;
+    const int nq = 2 * static_cast<int>(kstages(K));  // 1 KB runs per tile
+    const int row = 32 * static_cast<int>(blockIdx.x) + (lane & 31);
+    const bool row_ok = row < N;
+    const int nmine = nq > wave ? (nq - wave + GT_WAVES - 1) / GT_WAVES : 0;  // runs of this wave (uniform)
+    const uint8_t* wbase = Wt + static_cast<int64_t>(blockIdx.x) * nq * 1024 + 16 * lane;
+    float* sa_lds = reinterpret_cast<float*>(gv_lds + kb / 16);
+    uint16_t* sw_lds = reinterpret_cast<uint16_t*>(sa_lds + ng);  // [K/G][32]
+    // packed byte of A matching the lane's 16 weight bytes in run q
+    auto a_off = [&](int q) { return 64 * (q >> 1) + 32 * lh + 16 * (q & 1); };
+
+    uint4 w[GV_LOADS];
+    // runs i0 .. i0 + GV_LOADS - 1 of this wave (the zero padding past K and N
+    // loads like any other byte)
+    auto issue = [&](int i0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < GV_LOADS; ++j) {
+            const int q = wave + (i0 + j) * GT_WAVES;
+            w[j] = i0 + j < nmine ? *reinterpret_cast<const uint4*>(wbase + static_cast<int64_t>(q) * 1024)
+                                  : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+
+    issue(0);
+    // the tile's weight scales: the first GT_SWP per thread are loaded before A
+    // is staged and stored after, so their latency overlaps it; rows past N
+    // stage zeros (their sums are never stored)
+    const int64_t r0 = 32 * static_cast<int64_t>(blockIdx.x);
+    const int nsw = have_sc ? 32 * ng : 0;
+    auto sw_at = [&](int i) {
+        const int r = i / ng, g = i - r * ng;
+        return r0 + r < N ? sw[(r0 + r) * ng + g] : static_cast<uint16_t>(0);
+    };
+    uint16_t swv[GT_SWP];
+#pragma unroll
+    for (int u = 0; u < GT_SWP; ++u) swv[u] = tid + u * GT_NT < nsw ? sw_at(tid + u * GT_NT) : static_cast<uint16_t>(0);
+    gv_stage_a<FUSE, QL, GT_NT>(gv_lds, sa_lds, Aq, sa, have_sc, K, ng, x, aq_out, sa_out);
+#pragma unroll
+    for (int u = 0; u < GT_SWP; ++u) {
+        const int i = tid + u * GT_NT;
+        if (i < nsw) sw_lds[(i % ng) * 32 + i / ng] = swv[u];
+    }
+    for (int i = tid + GT_SWP * GT_NT; i < nsw; i += GT_NT) sw_lds[(i % ng) * 32 + i / ng] = sw_at(i);
+    __syncthreads();
+
+    float acc = 0.f;
+    for (int i0 = 0; i0 < nmine; i0 += GV_LOADS) {
+        if (i0 > 0) issue(i0);
+#pragma unroll
+        for (int j = 0; j < GV_LOADS; ++j) {
+            if (i0 + j < nmine) {  // uniform
+                const int off = a_off(wave + (i0 + j) * GT_WAVES);
+                if (off < kb) {
+                    const uint4 a = gv_lds[off >> 4];
+                    int p = __builtin_amdgcn_sdot8(static_cast<int>(a.x), static_cast<int>(w[j].x), 0, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.y), static_cast<int>(w[j].y), p, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.z), static_cast<int>(w[j].z), p, false);
+                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.w), static_cast<int>(w[j].w), p, false);
+                    if constexpr (DUMP) {
+                        if (pmr > 0 && row_ok) atomicAdd(&P[static_cast<int64_t>(row) * ng + ((2 * off) >> lgG)], p);
+                    }
+                    if (have_sc) {
+                        const int g = (2 * off) >> lgG;
+                        const float t = static_cast<float>(p) * sa_lds[g];
+                        acc = fmaf(t, gv_h2f(sw_lds[g * 32 + (lane & 31)]), acc);
+                    }
+                }
+            }
+        }
+    }
+    acc += __shfl_xor(acc, 32, 64);  // the row's two lane halves
+    if (lane < 32) red[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && lane < 32 && have_sc && row_ok) {
+        float v = red[0][lane];
+#pragma unroll
+        for (int u = 1; u < GT_WAVES; ++u) v += red[u][lane];
+        Y[row] = __half_as_ushort(__float2half_rn(v));
+    }
+}
+
 size_t gemv_lds_bytes(int64_t K, int64_t G) { return static_cast<size_t>(K / 2) + 4 * static_cast<size_t>(K / G); }
+// tiled: plus the tile's weight scales, binary16 [K/G][32]
+size_t gemv_tiled_lds_bytes(int64_t K, int64_t G) { return gemv_lds_bytes(K, G) + 64 * static_cast<size_t>(K / G); }
 
 // Rows per wave and workgroups: fill the load batch, but keep at least 8 waves
 // per CU when N allows.
@@ -206,27 +333,55 @@ GemvGrid gemv_grid(int64_t N, int64_t K) {
 template <bool FUSE, int QL>
 hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t N,
                          int64_t K, int64_t G, uint16_t* Y, const uint16_t* x, uint8_t* aq_out, uint16_t* sa_out,
-                         Dump dump, hipStream_t stream) {
-    const GemvGrid gg = gemv_grid(N, K);
+                         Dump dump, bool wt, hipStream_t stream) {
     int lgG = 31;
     if (G != K)
         for (lgG = 5; (int64_t{1} << lgG) < G; ++lgG) {
         }
-    const dim3 gd(static_cast<unsigned>(gg.grid)), bd(GV_NT);
     const size_t lds = gemv_lds_bytes(K, G);
-    const int n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G), rpw = static_cast<int>(gg.rpw);
+    const int n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
     if (dump.P) {
         // 32-code partial sums are added atomically into a zeroed window
         const hipError_t e = launch_fill_i32(dump.P, static_cast<int64_t>(dump.mr) * N * (K / G), 0, stream);
         if (e != hipSuccess) return e;
+    }
+    if (wt) {
+        const dim3 gd(static_cast<unsigned>((N + 31) / 32)), bd(GT_NT);
+        const size_t lds_t = gemv_tiled_lds_bytes(K, G);
+        // above 64 KB of dynamic LDS the kernel must allow it (at most
+        // 64 KB + K/2 <= 128 KB where gemv_fits holds and G >= 128)
+        static bool lds_attr_set = false;  // benign race: every caller sets the same value
+        if (!lds_attr_set) {
+            for (const void* kf : {reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, true>),
+                                   reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, false>)}) {
+                const hipError_t e = hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize, GT_MAX_LDS);
+                if (e != hipSuccess) return e;
+            }
+            lds_attr_set = true;
+        }
+        if (lds_t > GT_MAX_LDS) return hipErrorInvalidValue;
+        if (dump.P)
+            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, true>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, n, k, g,
+                               lgG, Y, x, aq_out, sa_out, dump.P, dump.mr);
+        else
+            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, false>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, n, k, g,
+                               lgG, Y, x, aq_out, sa_out, static_cast<int32_t*>(nullptr), 0);
+        return hipGetLastError();
+    }
+    const GemvGrid gg = gemv_grid(N, K);
+    const dim3 gd(static_cast<unsigned>(gg.grid)), bd(GV_NT);
+    const int rpw = static_cast<int>(gg.rpw);
+    if (dump.P)
         hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL, true>), gd, bd, lds, stream, Aq, sa, Wq, sw, n, k, g, lgG, rpw, Y, x,
                            aq_out, sa_out, dump.P, dump.mr);
-    } else {
+    else
         hipLaunchKernelGGL((w4a4_gemv_kernel<FUSE, QL, false>), gd, bd, lds, stream, Aq, sa, Wq, sw, n, k, g, lgG, rpw, Y,
                            x, aq_out, sa_out, static_cast<int32_t*>(nullptr), 0);
-    }
     return hipGetLastError();
 }
+
+// Workgroups of a one-row launch (row-major: rows-per-wave grid; tiled: one per 32 rows).
+int64_t gemv_workgroups(int64_t N, int64_t K, bool wt) { return wt ? (N + 31) / 32 : gemv_grid(N, K).grid; }
 
 }  // namespace
 
@@ -236,9 +391,9 @@ bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
 }
 
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump) {
-    if (!gemv_fits(M, N, K, G)) return hipErrorInvalidValue;
-    return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, dump, stream);
+                       int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump, bool wt) {
+    if (!gemv_fits(M, N, K, G) || (wt && G < 128)) return hipErrorInvalidValue;
+    return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, dump, wt, stream);
 }
 
 // Every workgroup quantizes all of x, so the fused prologue's total work is
@@ -246,23 +401,28 @@ hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
 // MI355X: 0.8 - 1.4 us faster at N = 1024 .. 10240, K = 8192), beyond it the
 // separate quantizer wins (0.9 us at N = 28672, 12 us at N = 8192, K = 28672).
 constexpr int64_t GV_FUSE_WORK = int64_t{1} << 23;
+// Tiled weights: 8-wave workgroups, and the fused form only paid up to
+// 256 x 8192 (MI355X: about even at N = 8192, K = 8192; 10 us slower at
+// N = 10240 and 20 us at N = 28672 than the quantizer and the GEMM).
+constexpr int64_t GT_FUSE_WORK = int64_t{1} << 21;
 
-bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G, bool wt) {
     return gemv_fits(M, N, K, G) && (G == 32 || G == 64 || G == 128 || G == 256 || G == 512) && G < K &&
-           gemv_grid(N, K).grid * K <= GV_FUSE_WORK;
+           !(wt && G < 128) && gemv_workgroups(N, K, wt) * K <= (wt ? GT_FUSE_WORK : GV_FUSE_WORK);
 }
 
 hipError_t launch_linear_fused(const uint16_t* x, const uint8_t* Wq, const uint16_t* sw, int64_t M, int64_t N, int64_t K,
-                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream, Dump dump) {
-    if (!fused_linear_fits(M, N, K, G)) return hipErrorInvalidValue;
+                               int64_t G, uint16_t* Y, uint8_t* Aq, uint16_t* sa, hipStream_t stream, Dump dump,
+                               bool wt) {
+    if (!fused_linear_fits(M, N, K, G, wt)) return hipErrorInvalidValue;
     const uint8_t* no_aq = nullptr;
     const uint16_t* no_sa = nullptr;
     switch (G) {
-        case 32: return launch_gemv_t<true, 4>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
-        case 64: return launch_gemv_t<true, 8>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
-        case 128: return launch_gemv_t<true, 16>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
-        case 256: return launch_gemv_t<true, 32>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
-        default: return launch_gemv_t<true, 64>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, stream);
+        case 32: return launch_gemv_t<true, 4>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, wt, stream);
+        case 64: return launch_gemv_t<true, 8>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, wt, stream);
+        case 128: return launch_gemv_t<true, 16>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, wt, stream);
+        case 256: return launch_gemv_t<true, 32>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, wt, stream);
+        default: return launch_gemv_t<true, 64>(no_aq, no_sa, Wq, sw, N, K, G, Y, x, Aq, sa, dump, wt, stream);
     }
 }
 

@@ -152,15 +152,48 @@ def test_debug_validation(L):
     assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, NULL, 0, s) == -1       # no P for a window
     assert f(*ok, 8, 8, 256, 128, NULL, *ws, 0, 8, h.ptr(), 0, s) == -1       # no Y
     assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 4, 5, h.ptr(), 0, s) == -2    # window past M
-    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, h.ptr(), 2, s) == -2    # unknown flag
+    assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, h.ptr(), 4, s) == -2    # unknown flag
     assert f(*ok, 8, 8, 256, 96, h.ptr(), *ws, 0, 8, h.ptr(), 0, s) == -3
     assert f(*ok, 8, 8, 256, 128, h.ptr(), *ws, 0, 8, h.ptr(4), 0, s) == -4   # misaligned P
     assert f(*ok, 8, 8, 256, 128, h.ptr(), h.ptr(8), 1 << 20, 0, 8, h.ptr(), 0, s) == -4
     g = L.apex4_w4a4_linear_debug
     args = [h.ptr()] * 3
-    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, NULL, s) == -1
-    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 2, 3, h.ptr(), s) == -2
-    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, h.ptr(8), s) == -4
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, NULL, 0, s) == -1
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 2, 3, h.ptr(), 0, s) == -2
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, h.ptr(), 1, s) == -2    # no general-tile flag
+    assert g(*args, 4, 8, 256, 64, h.ptr(), h.ptr(), h.ptr(), 0, 4, h.ptr(), 2, s) == -3     # tiled: G >= 128
+    assert g(*args, 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), 0, 4, h.ptr(8), 0, s) == -4
+
+
+def test_tiled_validation(L):
+    h = Host()
+    b = ctypes.c_int64(-1)
+    q = L.apex4_tiled_weights_size
+    assert q(8, 256, None) == -1
+    assert q(0, 256, ctypes.byref(b)) == -2
+    assert q(8, 48, ctypes.byref(b)) == -2 and b.value == -1
+    assert q(33, 160, ctypes.byref(b)) == 0 and b.value == 2 * 2 * 2048
+    t = L.apex4_tile_weights
+    s = NULL
+    assert t(NULL, 8, 256, h.ptr(), s) == -1
+    assert t(h.ptr(), 8, 256, NULL, s) == -1
+    assert t(h.ptr(), 8, 80, h.ptr(), s) == -2
+    assert t(h.ptr(), 1 << 20, 1 << 13, h.ptr(), s) == -2                # 4 GiB
+    assert t(h.ptr(4), 8, 256, h.ptr(), s) == -4
+    g = L.apex4_w4a4_gemm_tiled
+    ok = [h.ptr()] * 4
+    assert g(NULL, *ok[1:], 4, 8, 256, 128, h.ptr(), NULL, 0, s) == -1
+    assert g(*ok, 4, 8, 256, 64, h.ptr(), NULL, 0, s) == -3               # G < 128
+    assert g(*ok, 4, 8, 96, 96, h.ptr(), NULL, 0, s) == -3                # G == K < 128
+    assert g(*ok, 4, 8, 48, 48, h.ptr(), NULL, 0, s) == -2
+    assert g(h.ptr(2), *ok[1:], 4, 8, 8224, 8224, h.ptr(), NULL, 0, s) == -4   # G == K >= 128 accepted
+    assert g(*ok, 4, 8, 256, 128, h.ptr(), h.ptr(8), 64, s) == -4         # misaligned workspace
+    f = L.apex4_w4a4_linear_tiled
+    assert f(NULL, h.ptr(), h.ptr(), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -1
+    assert f(*[h.ptr()] * 3, 4, 8, 256, 32, h.ptr(), h.ptr(), h.ptr(), s) == -3
+    d = L.apex4_w4a4_gemm_debug
+    assert d(*ok, 8, 8, 256, 64, h.ptr(), NULL, 0, 0, 8, h.ptr(), 2, s) == -3   # tiled flag with G < 128
+    assert d(*ok, 8, 8, 256, 128, h.ptr(), NULL, 0, 0, 8, h.ptr(), 4, s) == -2  # unknown flag
 
 
 def test_plan_validation(L):
@@ -171,7 +204,8 @@ def test_plan_validation(L):
     assert f(0, 8, 8, 65568, 65568, 0, ctypes.byref(k), ctypes.byref(sp)) == -3
     assert f(3, 8, 8, 256, 128, 0, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown entry
     assert f(0, 8, 8, 256, 128, 4, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown flag
-    assert f(2, 8, 8, 256, 128, 1, ctypes.byref(k), ctypes.byref(sp)) == -2   # no flags for the linear
+    assert f(2, 8, 8, 256, 128, 1, ctypes.byref(k), ctypes.byref(sp)) == -2   # no general tiles for the linear
+    assert f(0, 8, 8, 256, 64, 2, ctypes.byref(k), ctypes.byref(sp)) == -3    # tiled needs G >= 128
     assert (k.value, sp.value) == (-9, -9)                                     # nothing written
 
 

@@ -317,31 +317,82 @@ def test_repeatable_and_degenerate():
     torch.cuda.synchronize()
 
 
+def _untile(Wt, N, K):
+    """Row-major packed codes back from the tiled layout (its definition, inverted)."""
+    T, S = -(-N // 32), -(-K // 128)
+    v = Wt.reshape(T, S, 2, 2, 32, 16)             # [t][s][j][h][c][b], lane = 32 h + c
+    rows = v.transpose(0, 4, 1, 3, 2, 5).reshape(T * 32, S * 64)
+    return rows[:N, :K // 2]
+
+
 def test_w4a4_linear_module(O):
-    """The drop-in layer: offline weight quantization + per-call activation
-    quantization and GEMM, batched leading dimensions, work buffers reused."""
+    """The drop-in layer: offline weight quantization (tiled layout by default,
+    row-major on request) + per-call activation quantization and GEMM, batched
+    leading dimensions, work buffers reused per (rows, stream)."""
     import torch
     m = pk()
     N, K, G = 1024, 2048, 128
     x, w = wl.float_workload("tiny", 64, N, K)
-    lin = m.W4A4Linear(dev(w), G)
     Wq_o, sw_o = O.quantize(w, G)
-    assert np.array_equal(host(lin.W_q), Wq_o)
+    lin = m.W4A4Linear(dev(w), G)
+    lin_r = m.W4A4Linear(dev(w), G, layout="rows")
+    assert lin.tiled and lin.W_q is None and not lin_r.tiled
+    assert np.array_equal(_untile(host(lin.W_t), N, K), Wq_o)
+    assert np.array_equal(host(lin_r.W_q), Wq_o)
+    stream = torch.cuda.current_stream()
     # same shape twice (buffers reused), then others; 64 rows take the split-K
     # GEMM with the layer's own workspace
     for rows in (24, 24, 7, 64):
         xb = x[:rows]
-        y = host(lin(dev(xb).reshape(1, rows, K)))
+        y = lin(dev(xb).reshape(1, rows, K))
+        yr = lin_r(dev(xb).reshape(1, rows, K))
+        torch.cuda.synchronize()
         assert y.shape == (1, rows, N)
-        assert (lin._work[2] is not None) == (rows == 64)
+        assert torch.equal(y, yr)                  # rows > 1: the same bits from either layout
+        assert (lin._work[(rows, stream.cuda_stream)][2] is not None) == (rows == 64)
         Aq_o, sa_o = O.quantize(xb, G)
-        check_tolerance(y[0], O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"module rows={rows}")
+        check_tolerance(host(y)[0], O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"module rows={rows}")
+    assert len(lin._work) == 3
+    # one row (the one-row kernels) through both layouts
+    y1, y1r = host(lin(dev(x[:1]))), host(lin_r(dev(x[:1])))
+    Aq_o, sa_o = O.quantize(x[:1], G)
+    for yy in (y1, y1r):
+        check_tolerance(yy, O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), "module one row")
     # per-channel weights through the same layer
     lin_c = m.W4A4Linear(dev(w), 0)
+    assert lin_c.tiled
     Wq_c, sw_c = O.quantize(w, K)
     Aq_c, sa_c = O.quantize(x[:24], K)
     check_tolerance(host(lin_c(dev(x[:24]))), O.gemm_rows(Aq_c, sa_c, Wq_c, sw_c, K, K), "module per-channel")
+    # G < 128 keeps row-major weights
+    lin_32 = m.W4A4Linear(dev(w), 32)
+    assert not lin_32.tiled
+    with pytest.raises(ValueError):
+        m.W4A4Linear(dev(w), 32, layout="tiled")
     torch.cuda.synchronize()
+
+
+def test_w4a4_linear_module_streams(O):
+    """Forwards with the same row count on two streams use separate work
+    buffers: both results are right although the streams overlap."""
+    import torch
+    m = pk()
+    N, K, G, rows = 2048, 4096, 128, 64
+    x, w = wl.float_workload("tiny", 2 * rows, N, K)
+    lin = m.W4A4Linear(dev(w), G)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    xa, xb = dev(x[:rows]), dev(x[rows:])
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        ya = lin(xa)
+    with torch.cuda.stream(s2):
+        yb = lin(xb)
+    torch.cuda.synchronize()
+    assert len(lin._work) == 2
+    Wq_o, sw_o = O.quantize(w, G)
+    for xx, yy in ((x[:rows], ya), (x[rows:], yb)):
+        Aq_o, sa_o = O.quantize(xx, G)
+        check_tolerance(host(yy), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), "module two streams")
 
 
 def test_weights_just_under_4gib(O):

@@ -179,7 +179,8 @@ class Quantized:
 
 def _linear_case(O, name, W, x, G, M):
     """P windows through apex4_w4a4_linear_debug and apex4_w4a4_gemm_debug (with
-    the workspace entry point's kernel choice), both against the oracle."""
+    the workspace entry point's kernel choice), both against the oracle, for
+    row-major and tiled weights (M >= 2: the same Y bits from either)."""
     import torch
     m = pk()
     N, K = W.q_o.shape[0], x.shape[1]
@@ -189,18 +190,26 @@ def _linear_case(O, name, W, x, G, M):
     plan_ws = m.apex4_w4a4_gemm_plan("gemm_ws", M, N, K, G)
     log(f"{name}: linear {plan_lin}, gemm_ws {plan_ws}")
     xd = dev(x)
+    Wt = m.apex4_tile_weights(W.q_d)
+    T = m.APEX4_DEBUG_W_TILED
     Y_lin = m.apex4_w4a4_linear(xd, W.q_d, W.s_d, G)
     Y_ws = m.apex4_w4a4_gemm_ws(A.q_d, A.s_d, W.q_d, W.s_d, G, ws)
+    Y_lin_t = m.apex4_w4a4_linear_tiled(xd, Wt, W.s_d, G)
+    Y_ws_t = m.apex4_w4a4_gemm_tiled(A.q_d, A.s_d, Wt, W.s_d, G, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Y_lin_t, Y_lin) and torch.equal(Y_ws_t, Y_ws), name
     for m0, mr in windows(M):
         P_o = O.groupsums(A.q_o, W.q_o, K, G, m0, mr)
         Yl, Aw, sw_, Pl = m.apex4_w4a4_linear_debug(xd, W.q_d, W.s_d, G, m0, mr)
         Yw, Pw = m.apex4_w4a4_gemm_debug(A.q_d, A.s_d, W.q_d, W.s_d, G, m0, mr, workspace=ws)
+        Ylt, _, _, Plt = m.apex4_w4a4_linear_debug(xd, Wt, W.s_d, G, m0, mr, flags=T)
+        Ywt, Pwt = m.apex4_w4a4_gemm_debug(A.q_d, A.s_d, Wt, W.s_d, G, m0, mr, workspace=ws, flags=T)
         torch.cuda.synchronize()
-        assert torch.equal(Yl, Y_lin), (name, m0)
-        assert torch.equal(Yw, Y_ws), (name, m0)
+        assert torch.equal(Yl, Y_lin) and torch.equal(Ylt, Y_lin), (name, m0)
+        assert torch.equal(Yw, Y_ws) and torch.equal(Ywt, Y_ws), (name, m0)
         assert torch.equal(Aw, A.q_d) and torch.equal(sw_.view(torch.int16), A.s_d.view(torch.int16))
-        assert np.array_equal(host(Pl), P_o), (name, "linear", m0, mr)
-        assert np.array_equal(host(Pw), P_o), (name, "gemm_ws", m0, mr)
+        for tag, Pd in (("linear", Pl), ("gemm_ws", Pw), ("linear tiled", Plt), ("gemm_ws tiled", Pwt)):
+            assert np.array_equal(host(Pd), P_o), (name, tag, m0, mr)
     rows = np.unique(np.concatenate([np.arange(w0, w0 + wr) for w0, wr in windows(M)]))
     y = O.gemm_rows(A.q_o, A.s_o, W.q_o, W.s_o, K, G, rows)
     check_tolerance(host(Y_lin)[rows], y, f"{name} linear")
@@ -263,11 +272,23 @@ def test_decode_linear_groupsums(O, N, K):
         Y = m.apex4_w4a4_linear(dev(x), W.q_d, W.s_d, G)
         Yl, _, _, Pl = m.apex4_w4a4_linear_debug(dev(x), W.q_d, W.s_d, G)
         Yg, Pg = m.apex4_w4a4_gemm_debug(A.q_d, A.s_d, W.q_d, W.s_d, G)
+        # the tiled layout: the same kernels' tiled forms
+        Wt = m.apex4_tile_weights(W.q_d)
+        T = m.APEX4_DEBUG_W_TILED
+        log(f"decode N={N} K={K} M={M} tiled: {m.apex4_w4a4_gemm_plan('linear', M, N, K, G, T)}")
+        Yt = m.apex4_w4a4_linear_tiled(dev(x), Wt, W.s_d, G)
+        Ylt, _, _, Plt = m.apex4_w4a4_linear_debug(dev(x), Wt, W.s_d, G, flags=T)
+        Ygt, Pgt = m.apex4_w4a4_gemm_debug(A.q_d, A.s_d, Wt, W.s_d, G, flags=T)
         torch.cuda.synchronize()
         assert torch.equal(Yl, Y) and torch.equal(Yg, Y)
-        assert np.array_equal(host(Pl), P_o)
-        assert np.array_equal(host(Pg), P_o)
-        check_tolerance(host(Y), O.gemm_rows(A.q_o, A.s_o, W.q_o, W.s_o, K, G), f"decode M={M}")
+        assert torch.equal(Ylt, Yt) and torch.equal(Ygt, Yt)
+        if M > 1:
+            assert torch.equal(Yt, Y)
+        for Pd in (Pl, Pg, Plt, Pgt):
+            assert np.array_equal(host(Pd), P_o)
+        y = O.gemm_rows(A.q_o, A.s_o, W.q_o, W.s_o, K, G)
+        check_tolerance(host(Y), y, f"decode M={M}")
+        check_tolerance(host(Yt), y, f"decode tiled M={M}")
 
 
 # the decode and one-row kernels at every G, sub-group partials (G > 128) included

@@ -166,6 +166,7 @@ def test_linear_module_mx():
     """W4A4Linear(scales="mx"): weights quantized once with power-of-two scales,
     activations per call, against the oracle's MX quantize + GEMM (these row
     counts take the split-K form with the layer's own workspace)."""
+    import torch
     m = pk()
     N, K, G = 1024, 2048, 64
     x, w = wl.float_workload("tiny", 64, N, K)
@@ -176,7 +177,8 @@ def test_linear_module_mx():
     for rows in (5, 64, 64):
         y = host(lin(dev(x[:rows]).reshape(1, rows, K)))
         assert y.shape == (1, rows, N)
-        assert (lin._work[2] is not None) == (m.apex4_w4a4_gemm_mx_workspace_size(rows, N, K, G) > 0)
+        key = (rows, torch.cuda.current_stream().cuda_stream)
+        assert (lin._work[key][2] is not None) == (m.apex4_w4a4_gemm_mx_workspace_size(rows, N, K, G) > 0)
         Aq_o, ea_o = omx.quantize_mx(x[:rows], G)
         check_tolerance(y[0], omx.gemm_mx_f64(Aq_o, ea_o, Wq_o, ew_o, K, G), f"mx module rows={rows}")
     with pytest.raises(ValueError):
