@@ -696,13 +696,15 @@ def summarize_gsweep(trace_csv, pmc_csv, cmds):
 
 
 def counters_mode():
-    """Launch the paper-shape GEMM 3 times and a 256 MiB reference copy 3 times,
-    nothing else, so that per-dispatch counters of both can be compared."""
+    """Launch the paper-shape GEMM (tiled weights, as the bench times it) 3 times
+    and a 256 MiB reference copy 3 times, nothing else, so that per-dispatch
+    counters of both can be compared."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import rho, workloads as wl
     dev = torch.device("cuda", 0)
     c = [torch.from_numpy(a).to(dev) for a in wl.codes_workload("paper", M, N, K, G)]
+    Wt = pk.apex4_tile_weights(c[2])                 # the bench's weight layout
     Y = torch.empty((M, N), dtype=torch.float16, device=dev)
     src = torch.randint(0, 255, (256 << 20,), dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
@@ -710,7 +712,7 @@ def counters_mode():
     for _ in range(3):
         rho.copy(src, dst)
     for _ in range(3):
-        pk.apex4_w4a4_gemm(*c, G, Y)
+        pk.apex4_w4a4_gemm_tiled(c[0], c[1], Wt, c[3], G, Y=Y)
     torch.cuda.synchronize()
     print(json.dumps({"mode": "counters", "copy_bytes": 256 << 20, "gemm": [M, N, K, G],
                       "gemm_algorithmic_bytes": M * K // 2 + N * K // 2 + 2 * (M + N) * (K // G) + 2 * M * N}))
@@ -900,9 +902,10 @@ def decode_counters_mode():
     """A 256 MiB reference copy 3 times, then each DECODE_TRAFFIC linear
     (apex4_w4a4_linear_tiled from fp16 x: the fused one-row kernel where it
     applies, else the quantizer and the GEMM) DECODE_TRAFFIC_REPS times, on
-    tiled weight copies rotated past the 256 MB cache.  All inputs are made
-    first, so the only kernels launched in order are these; the printed launch
-    list maps profiler dispatches to cases."""
+    tiled weight copies rotated past the 256 MB cache (after one pass over
+    every copy).  All inputs are made and that pass is done first, so the
+    kernels after the first copy are exactly these, in order; the printed
+    launch list maps profiler dispatches to cases."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import rho, workloads as wl
@@ -925,6 +928,11 @@ def decode_counters_mode():
                 torch.empty((Md, Kd // Gd), dtype=torch.float16, device=dev))
         kern, _ = pk.apex4_w4a4_gemm_plan("linear", Md, Nd, Kd, Gd, pk.APEX4_DEBUG_W_TILED)
         cases.append((label, Md, Nd, Kd, kern, x, Wts, sw, bufs))
+    # one untraced pass over every copy (address translation warm), in the
+    # rotation order, so each traced launch reads weights evicted from the cache
+    for (label, Md, Nd, Kd, kern, x, Wts, sw, (Y, Aq, sa)) in cases:
+        for Wt in Wts:
+            pk.apex4_w4a4_linear_tiled(x, Wt, sw, Gd, Y, Aq, sa)
     torch.cuda.synchronize()
     launches = []
     for _ in range(3):
@@ -950,8 +958,9 @@ def _decode_kernel_role(name: str):
         return "copy"
     if "quant_small_kernel" in name or "quant_large_kernel" in name:
         return "quant"
-    if "w4a4_gemv_kernel" in name:
-        return "fused" if re.search(r"w4a4_gemv_kernel<true", name) else "gemv"
+    m = re.search(r"w4a4_gemv(?:_tiled)?_kernel<(true|false)", name)
+    if m:
+        return "fused" if m.group(1) == "true" else "gemv"
     if "w4a4_decode_kernel" in name:
         return "decode"
     if is_tiled_gemm(name):
@@ -1005,7 +1014,8 @@ def summarize_decode_traffic(args):
              "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
              "`bench.py --mode decode_counters` runs a 256 MiB reference copy 3 times, then each linear",
              "(`apex4_w4a4_linear_tiled` from fp16 x, G = 128: the fused one-row kernel where the library picks",
-             "it, else the quantizer and the GEMM) 3 times, on tiled weight copies rotated past the 256 MB cache.",
+             "it, else the quantizer and the GEMM) 3 times, on tiled weight copies rotated past the 256 MB cache",
+             "(every copy is used once, untraced, before the reference copy).",
              "FETCH_SIZE and WRITE_SIZE",
              "(KiB per dispatch) are scaled by what they read for the copy "
              f"(read scale {fs:.3f}, write scale {ws:.3f}).  Duration: kernel trace of a separate run of the same",
