@@ -9,7 +9,9 @@ division and square root stay correctly rounded (the quantizer relies on it).
 from __future__ import annotations
 
 import glob
+import json
 import os
+import re
 import subprocess
 import sys
 
@@ -18,6 +20,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libapex4.so")
+# per-kernel registers and scratch of the last build (the compiler's resource remarks)
+RESOURCES = os.path.join(HERE, "kernel_resources.json")
 RHO_SRC = os.path.join(HERE, "rho", "rho_probe.hip")
 RHO_LIB = os.path.join(HERE, "librho_apex4.so")
 
@@ -42,13 +46,37 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def _hipcc(srcs: list[str], out: str, verbose: bool) -> None:
-    cmd = [HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", *srcs, "-o", out + ".tmp"]
+def _resources(stderr: str) -> dict:
+    """{kernel: {"vgpr": n, "agpr": n, "scratch": bytes per lane, "occupancy": waves per SIMD}}
+    from -Rpass-analysis=kernel-resource-usage remarks."""
+    res, name = {}, None
+    keys = {"VGPRs": "vgpr", "AGPRs": "agpr", "ScratchSize [bytes/lane]": "scratch", "Occupancy [waves/SIMD]": "occupancy"}
+    for line in stderr.splitlines():
+        m = re.search(r"remark: .*?Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            res.setdefault(name, {})
+            continue
+        m = re.search(r"remark: .*?\s(VGPRs|AGPRs|ScratchSize \[bytes/lane\]|Occupancy \[waves/SIMD\]): (\d+)", line)
+        if m and name:
+            res[name][keys[m.group(1)]] = int(m.group(2))
+    return res
+
+
+def _hipcc(srcs: list[str], out: str, verbose: bool, resources: str | None = None) -> None:
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if resources else []
+    cmd = [HIPCC, *HIP_FLAGS, *extra, f"-I{INCLUDE}", f"-I{CSRC}", *srcs, "-o", out + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
-    # hipcc's host pass does not know the packed-fp32 feature and says so; that is harmless
-    err = "\n".join(l for l in res.stderr.splitlines() if "packed-fp32-ops" not in l and l.strip())
+    if resources and res.returncode == 0:
+        with open(resources, "w") as f:
+            json.dump(_resources(res.stderr), f, indent=0, sort_keys=True)
+    # hipcc's host pass does not know the packed-fp32 feature and says so; that
+    # is harmless; the resource remarks went to the file above
+    err = "\n".join(l for l in res.stderr.splitlines()
+                    if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l and l.strip()
+                    and not re.match(r"^\s*\d*\s*\|", l))
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err:
@@ -58,7 +86,7 @@ def _hipcc(srcs: list[str], out: str, verbose: bool) -> None:
 
 def build(verbose: bool = False) -> str:
     """Build libapex4.so (the product) and librho_apex4.so (the rho probes)."""
-    _hipcc(sources(), LIB, verbose)
+    _hipcc(sources(), LIB, verbose, RESOURCES)
     _hipcc([RHO_SRC], RHO_LIB, verbose)
     return LIB
 

@@ -141,10 +141,13 @@ __device__ __forceinline__ i32x16 splat16(int v) {
 // to P[pmr][N][K/G] as each group completes (the Y path is unchanged; with
 // sa == nullptr the scales are not read and Y is not written).
 //
-// K need not be a multiple of 128 (groups of 32 or 64, or G = K): the last
-// stage is then partial, and its missing codes load as zeros, which add
-// nothing to any sum; its missing groups are neither dequantized nor dumped.
-template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF, int KSPLIT, bool DUMP>
+// TAIL: K is not a multiple of 128 (groups of 32 or 64, or G = K): the last
+// stage is partial, its missing codes load as zeros, which add nothing to any
+// sum, and its missing groups are neither dequantized nor dumped.  Only the
+// TAIL instantiations carry the masks: with them in the steady-state code
+// the register allocation spilled (up to 900 bytes per lane at G = 32).
+template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int GPS, int PF, int KSPLIT, bool DUMP,
+          bool TAIL>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
@@ -206,7 +209,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     // Rows past M or N are clamped to the last row: they only feed outputs that
     // are never stored, so loads need no branch.
     uint32_t a_off[A_CH];
-    int a_lds0[A_CH], a_lds1[A_CH], a_pos[A_CH];
+    int a_lds0[A_CH], a_lds1[A_CH];
+    [[maybe_unused]] int a_pos[A_CH];
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
         const int c = tid + i * NT;
@@ -260,7 +264,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Aq + static_cast<int64_t>(ks) * (KS / 2);
         const int lim = kb - ks * (KS / 2);  // packed bytes of this stage inside the row (uniform)
-        if (lim >= KS / 2) {
+        if (!TAIL || lim >= KS / 2) {
 #pragma unroll
             for (int i = 0; i < A_CH; ++i) ra[sl][i] = *reinterpret_cast<const uint4*>(base + a_off[i]);
         } else {
@@ -278,7 +282,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
             const uint16_t* sp = sc_base + sc_off + static_cast<uint32_t>(g0);
             if constexpr (GPS == 1) {
                 rsc[sl][0] = *sp;
-            } else if ((ng % GPS) == 0) {
+            } else if (!TAIL || (ng % GPS) == 0) {
                 if constexpr (GPS == 2) {
                     const uint32_t v = *reinterpret_cast<const uint32_t*>(sp);
                     rsc[sl][0] = static_cast<uint16_t>(v);
@@ -312,25 +316,45 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         constexpr int sl = decltype(SLOT)::value;
         const uint8_t* base = Wq + static_cast<int64_t>(ks) * w_sstride;
         const int lim = kb - ks * (KS / 2);  // uniform
-        const bool full = tiled || lim >= KS / 2;  // the tiled layout is zero padded
-        const uint2 z2 = make_uint2(0u, 0u);
+        // full stages (and the zero-padded tiled layout) load unmasked; only a
+        // partial last stage takes the per-lane masks (a branch on a uniform
+        // value, so the full-stage code carries no selects)
+        if (!TAIL || tiled || lim >= KS / 2) {
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            if constexpr (FINE) {
-                // MFMA kk, lane half h: packed bytes 16 kk + 8 h .. + 7
-                const uint8_t* q = base + w_off[j];
-                const int h8 = 8 * lh;
-                const uint2 q0 = (full || h8 < lim) ? *reinterpret_cast<const uint2*>(q) : z2;
-                const uint2 q1 = (full || 16 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 16) : z2;
-                const uint2 q2 = (full || 32 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 32) : z2;
-                const uint2 q3 = (full || 48 + h8 < lim) ? *reinterpret_cast<const uint2*>(q + 48) : z2;
-                w[sl][j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
-                w[sl][j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
-            } else {
-                const int h32 = 32 * lh;
-                w[sl][j][0] = (full || h32 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j]) : make_uint4(0u, 0u, 0u, 0u);
-                w[sl][j][1] = (full || h32 + 16 < lim) ? *reinterpret_cast<const uint4*>(base + w_off[j] + w_jstride)
-                                                       : make_uint4(0u, 0u, 0u, 0u);
+            for (int j = 0; j < NJ; ++j) {
+                if constexpr (FINE) {
+                    // MFMA kk, lane half h: packed bytes 16 kk + 8 h .. + 7
+                    const uint8_t* q = base + w_off[j];
+                    const uint2 q0 = *reinterpret_cast<const uint2*>(q);
+                    const uint2 q1 = *reinterpret_cast<const uint2*>(q + 16);
+                    const uint2 q2 = *reinterpret_cast<const uint2*>(q + 32);
+                    const uint2 q3 = *reinterpret_cast<const uint2*>(q + 48);
+                    w[sl][j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+                    w[sl][j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+                } else {
+                    w[sl][j][0] = *reinterpret_cast<const uint4*>(base + w_off[j]);
+                    w[sl][j][1] = *reinterpret_cast<const uint4*>(base + w_off[j] + w_jstride);
+                }
+            }
+        } else {
+            const uint2 z2 = make_uint2(0u, 0u);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                if constexpr (FINE) {
+                    const uint8_t* q = base + w_off[j];
+                    const int h8 = 8 * lh;
+                    const uint2 q0 = h8 < lim ? *reinterpret_cast<const uint2*>(q) : z2;
+                    const uint2 q1 = 16 + h8 < lim ? *reinterpret_cast<const uint2*>(q + 16) : z2;
+                    const uint2 q2 = 32 + h8 < lim ? *reinterpret_cast<const uint2*>(q + 32) : z2;
+                    const uint2 q3 = 48 + h8 < lim ? *reinterpret_cast<const uint2*>(q + 48) : z2;
+                    w[sl][j][0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+                    w[sl][j][1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+                } else {
+                    const int h32 = 32 * lh;
+                    w[sl][j][0] = h32 < lim ? *reinterpret_cast<const uint4*>(base + w_off[j]) : make_uint4(0u, 0u, 0u, 0u);
+                    w[sl][j][1] = h32 + 16 < lim ? *reinterpret_cast<const uint4*>(base + w_off[j] + w_jstride)
+                                                 : make_uint4(0u, 0u, 0u, 0u);
+                }
             }
         }
     };
@@ -944,6 +968,8 @@ template <int WAVES_M, int WAVES_N, int MI, int NJ, int MODE, bool MAGIC_OK, int
 hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                     int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
                     void* part = nullptr) {
+    // a partial last stage only happens with groups finer than a stage or one group per row
+    constexpr bool can_tail = GPS > 1 || MODE == kChannel;
     constexpr int BM = WAVES_M * MI * 32, BN = WAVES_N * NJ * 32;
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
@@ -952,11 +978,20 @@ hipError_t launch_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, co
     // M = 64..256, N = 8192 for G in {128, 256}, 24 % for G = K).  With G < 128
     // the deeper ring costs occupancy and time, so those keep one stage.
     constexpr int PF = (WAVES_M * WAVES_N * MI * NJ <= 8 && GPS == 1) ? 4 : 1;
-    hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT, DUMP>),
-                       dim3(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), dim3(64 * WAVES_M * WAVES_N * KSPLIT),
-                       0, stream, Aq, sa, Wq, sw, static_cast<int>(M), static_cast<int>(N), static_cast<int>(K),
-                       static_cast<int>(G), Y, dump.P, dump.m0, dump.mr, static_cast<int>(kstages(K) / S), part,
-                       wt ? 1 : 0);
+    const dim3 grid(static_cast<unsigned>(tiles), static_cast<unsigned>(S)), block(64 * WAVES_M * WAVES_N * KSPLIT);
+    const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
+    const int nks = static_cast<int>(kstages(K) / S), w = wt ? 1 : 0;
+    if (K % KS != 0) {
+        if constexpr (can_tail)
+            hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT, DUMP, true>),
+                               grid, block, 0, stream, Aq, sa, Wq, sw, m, n, k, g, Y, dump.P, dump.m0, dump.mr, nks, part,
+                               w);
+        else
+            return hipErrorInvalidValue;
+    } else {
+        hipLaunchKernelGGL((w4a4_gemm_kernel<WAVES_M, WAVES_N, MI, NJ, MODE, MAGIC_OK, GPS, PF, KSPLIT, DUMP, false>),
+                           grid, block, 0, stream, Aq, sa, Wq, sw, m, n, k, g, Y, dump.P, dump.m0, dump.mr, nks, part, w);
+    }
     return hipGetLastError();
 }
 

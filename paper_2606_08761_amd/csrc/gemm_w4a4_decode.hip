@@ -78,7 +78,9 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
 // are dequantized and reduced.  PF: stages in flight per wave.  GPS: groups per
 // 128-wide stage (1 for G >= 128, 2 for G = 64, 4 for G = 32).  Lane l holds
 // rows 8 (r / 4) + 4 (l / 32) + r % 4 for r < MROWS / 2.
-template <int MROWS, int PF, int GPS, bool DUMP>
+// TAIL: K % 128 != 0, the last stage is partial and its loads are masked
+// (only then: the masks cost selects on every load).
+template <int MROWS, int PF, int GPS, bool DUMP, bool TAIL>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
@@ -236,7 +238,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const int s = min(wave + NWAVE * li, nks - 1);
         const uint8_t* wb = Wq + static_cast<int64_t>(s) * w_sstride;
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
-        const int lim = kb - s * 64;
+        const int lim = TAIL ? kb - s * 64 : 64;
         load32(wb + w_voff, rw[j], tiled ? 64 : lim, w_jstride);  // the tiled layout is zero padded
         load32(ab + a_voff, ra[j], lim, 16);
         if (++li == per_tile) {
@@ -364,14 +366,14 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     }
 }
 
-template <int PF, int GPS, bool DUMP>
+template <int PF, int GPS, bool DUMP, bool TAIL>
 hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                             int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
     static bool lds_attr_set = false;  // benign race: every caller sets the same value
     if (!lds_attr_set) {
-        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS, DUMP>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS, DUMP>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS, DUMP>)}) {
+        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS, DUMP, TAIL>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS, DUMP, TAIL>),
+                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS, DUMP, TAIL>)}) {
             const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * MAX_SC_LDS);
             if (e != hipSuccess) return e;
         }
@@ -384,25 +386,29 @@ hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
     const int w = wt ? 1 : 0;
     if (M <= 8)
-        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
-                           dump.P, dump.m0, dump.mr, w);
+        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
+                           Y, dump.P, dump.m0, dump.mr, w);
     else if (M <= 16)
-        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
-                           dump.P, dump.m0, dump.mr, w);
+        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
+                           Y, dump.P, dump.m0, dump.mr, w);
     else
-        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS, DUMP>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g, Y,
-                           dump.P, dump.m0, dump.mr, w);
+        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
+                           Y, dump.P, dump.m0, dump.mr, w);
     return hipGetLastError();
 }
 
 template <int PF, int GPS>
 hipError_t launch_decode_g(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                            int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
-    if (!dump.P) return launch_decode_pf<PF, GPS, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream);
+    const bool tail = K % 128 != 0;
+    if (!dump.P)
+        return tail ? launch_decode_pf<PF, GPS, false, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream)
+                    : launch_decode_pf<PF, GPS, false, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream);
     // partial sums are added atomically into a zeroed window
     const hipError_t e = launch_fill_i32(dump.P, static_cast<int64_t>(dump.mr) * N * (K / G), 0, stream);
     if (e != hipSuccess) return e;
-    return launch_decode_pf<PF, GPS, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream);
+    return tail ? launch_decode_pf<PF, GPS, true, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream)
+                : launch_decode_pf<PF, GPS, true, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream);
 }
 
 }  // namespace
