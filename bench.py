@@ -285,8 +285,9 @@ def layers_mode(reps: int = 10):
     copies (twice the Infinity Cache); codes and scales are random (speed does
     not depend on values).  The W4A4 linears are timed from a replayed graph of
     `reps` calls (GPU time, no Python launch overhead), the fp16 GEMMs eagerly.
-    Where the G=128 GEMM is split over K the linear is the quantizer followed by
-    apex4_w4a4_gemm_ws with a workspace, as W4A4Linear runs it."""
+    Each linear runs as W4A4Linear runs it: weights in the tiled layout for
+    G >= 128 (row-major below), the linear entry point, or the quantizer
+    followed by the GEMM split over K with a workspace where that applies."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import workloads as wl
@@ -333,6 +334,8 @@ def layers_mode(reps: int = 10):
         for name, Nl, Kl, Gl in linears:
             Gv = Gl or Kl
             Wq = torch.from_numpy(wl.random_codes(r, Nl, Kl)).to(dev)
+            if Gv >= 128:
+                Wq = pk.apex4_tile_weights(Wq)
             sw = torch.from_numpy(wl.random_scales(r, Nl, Kl // Gv)).to(dev)
             R = copies(Nl * Kl // 2 + 2 * Nl * (Kl // Gv))
             wsets[name] = [(Wq, sw)] + [(Wq.clone(), sw.clone()) for _ in range(R - 1)]
@@ -346,16 +349,20 @@ def layers_mode(reps: int = 10):
                 sa = torch.empty((Ml, Kl // Gv), dtype=torch.float16, device=dev)
                 ws = wsets[name]
                 need = pk.apex4_w4a4_gemm_workspace_size(Ml, Nl, Kl, Gv)
+                tiled = Gv >= 128
                 if need:
                     # as W4A4Linear: quantize, then the GEMM split over K with a workspace
                     work = torch.empty((need,), dtype=torch.uint8, device=dev)
+                    gemm = pk.apex4_w4a4_gemm_tiled if tiled else pk.apex4_w4a4_gemm_ws
 
                     def call(i):
                         pk.apex4_quantize_act(x, Gv, Aq, sa)
-                        pk.apex4_w4a4_gemm_ws(Aq, sa, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, work, Y)
+                        gemm(Aq, sa, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, work, Y)
                 else:
+                    linear = pk.apex4_w4a4_linear_tiled if tiled else pk.apex4_w4a4_linear
+
                     def call(i):
-                        pk.apex4_w4a4_linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa)
+                        linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa)
                 t = graph_timed(call, reps)
                 split[name] = need // (4 * Ml * Nl) if need else 1
                 per[name] = round(t, 2)
@@ -420,9 +427,10 @@ def summarize_layers(path, command):
     tot = {(r["config"], r["M"]): r for r in rows}
     lines = ["# Llama-2-70B decoder-layer linears: uniform G=128 vs mixed granularity vs fp16", "",
              "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
-             "Each W4A4 linear is timed as quantize + GEMM from fp16 activations (apex4_w4a4_linear, or "
-             "apex4_quantize_act + apex4_w4a4_gemm_ws where the G=128 GEMM is split over K into S "
-             "ranges, marked S=) from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
+             "Each W4A4 linear is timed as W4A4Linear runs it: quantize + GEMM from fp16 activations "
+             "(apex4_w4a4_linear_tiled on tiled weights for G >= 128, apex4_w4a4_linear on row-major weights "
+             "below; or the quantizer + the GEMM split over K into S ranges with a workspace, marked S=) "
+             "from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
              "torch.matmul (hipBLASLt) on the same shapes, rotated the same way, timed eagerly. "
              "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
              "share one per-channel GEMM (N=9216).", "",
