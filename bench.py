@@ -236,14 +236,18 @@ def summarize_mode(args):
                   "Linear = apex4_w4a4_linear from fp16 x (one fused kernel at M=1 where it pays, quantizer + GEMM otherwise); "
                   "quantize then GEMM = the two entry points called in turn.", "",
                   "Weights in the tiled layout; the row-major column runs the same GEMM on row-major weights.", "",
+                  "Plain read = a streaming read kernel (librho_apex4 apex4_read_probe) over the same rotated "
+                  "weight copies, graph-timed the same way: the rate any kernel that reads those bytes once "
+                  "reaches at that size; GEMM / read = read time / GEMM time.", "",
                   "| decode M | N | K | kernel | linear us (eager / graph) | quantize then GEMM us (graph) | "
-                  "GEMM us (eager / graph) | GEMM HBM GB/s (fraction of 8 TB/s) | row-major GEMM us (graph) | "
-                  "fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
-                  "|---|---|---|---|---|---|---|---|---|---|---|"]
+                  "GEMM us (eager / graph) | GEMM HBM GB/s (fraction of 8 TB/s) | plain read us (fraction of 8 TB/s) | "
+                  "GEMM / read | row-major GEMM us (graph) | fp16 GEMM us (eager) | linear speedup vs fp16 (eager / graph) |",
+                  "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
         for d in b.get("decode", []):
             lines.append(f"| {d['M']} | {d['N']} | {d['K']} | {d.get('kernel')} | {d['linear_us']} / {d.get('linear_graph_us')} | "
                          f"{d.get('quant_then_gemm_graph_us')} | {d['gemm_us']} / {d.get('gemm_graph_us')} | "
-                         f"{d['gemm_hbm_gbs']} ({d['gemm_hbm_frac']}) | {d.get('row_major_gemm_graph_us')} | "
+                         f"{d['gemm_hbm_gbs']} ({d['gemm_hbm_frac']}) | {d.get('read_graph_us')} ({d.get('read_hbm_frac')}) | "
+                         f"{d.get('gemm_rate_vs_read')} | {d.get('row_major_gemm_graph_us')} | "
                          f"{d['fp16_gemm_us']} | {d['speedup_linear_vs_fp16']} / {d.get('speedup_linear_graph_vs_fp16')} |")
     with open(os.path.join(ROOT, "profiles", "gemm_w4a4_paper_shape.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -782,7 +786,8 @@ def gsweep_mode(reps: int = 20):
 
 # (M, N, K): Llama-2-70B o_proj-sized (8192 x 8192), gate/up-sized (28672 x
 # 8192) and down (8192 x 28672) linears at decode batch sizes
-DECODE_CASES = [(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)] + [(1, 8192, 28672), (8, 8192, 28672)]
+DECODE_CASES = ([(M_, N_, 8192) for N_ in (8192, 28672) for M_ in (1, 8, 32)] + [(1, 8192, 28672), (8, 8192, 28672)] +
+                [(16, 10240, 8192), (16, 8192, 8192), (16, 57344, 8192), (16, 8192, 28672)])  # Llama-2-70B at M = 16
 
 
 def decode_bench(reps: int = 50):
@@ -799,6 +804,7 @@ def decode_bench(reps: int = 50):
     """
     import torch
     import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import rho as rho_probe
     from paper_2606_08761_amd import workloads as wl
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream(dev)
@@ -877,6 +883,11 @@ def decode_bench(reps: int = 50):
         # entry point runs unless its one-row fused kernel pays
         two = lambda i: (pk.apex4_quantize_act(x, Gd, Aq, sa), gem(i))
         two_g_us = graph_timed(two, Y)
+        # a plain streaming read of the same weight copies: the speed any kernel
+        # that reads these bytes once reaches at this size (the practical roofline)
+        sink = torch.zeros(1024, dtype=torch.int32, device=dev)
+        read_g_us = graph_timed(lambda i: rho_probe.read(tsets[i % nq], sink), sink)
+        read_bytes = tsets[0].numel()
         yf = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
         fp16_us = timed(lambda i: torch.matmul(x, fsets[i % len(fsets)].t(), out=yf))
         gbytes = Md * Kd / 2 + Nd * Kd / 2 + 2 * (Md + Nd) * Kd / Gd + 2 * Md * Nd
@@ -889,6 +900,9 @@ def decode_bench(reps: int = 50):
                     "kernel": pk.apex4_w4a4_gemm_plan("linear", Md, Nd, Kd, Gd, pk.APEX4_DEBUG_W_TILED)[0],
                     "row_major_linear_graph_us": round(lin_r_g_us, 2), "row_major_gemm_graph_us": round(gemm_r_g_us, 2),
                     "row_major_gemm_hbm_frac": round(gbytes / (gemm_r_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
+                    "read_graph_us": round(read_g_us, 2),
+                    "read_hbm_frac": round(read_bytes / (read_g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3),
+                    "gemm_rate_vs_read": round(read_g_us / gemm_g_us, 3),
                     "fp16_gemm_us": round(fp16_us, 2), "speedup_linear_vs_fp16": round(fp16_us / lin_us, 3),
                     "speedup_linear_graph_vs_fp16": round(fp16_us / lin_g_us, 3)})
         del x, Aq, sa, Y, yf

@@ -38,6 +38,17 @@
 //     1 KB), instead of 64 bytes from each of 32 rows (measured on MI355X with
 //     the weights rotated past the 256 MB cache: 5-20 % less time at
 //     M = 8..32, N = 8192..57344).
+//   * Activations in LDS (ALDS): when K % 512 == 0 and the M packed rows fit
+//     beside the scales, the workgroup stages them in LDS once, straight from
+//     global memory (global_load_lds, no registers; 16-byte chunks swizzled
+//     per row so the rows of a fragment read spread over the banks), and each
+//     stage reads its fragment there instead of from global memory.  Every
+//     wave otherwise re-reads the activations for each of its tiles, as many
+//     requests as the weights (measured on MI355X: 8-23 % of the time at
+//     M = 16..32).
+//   * The 8 partial fp32 tiles are reduced through LDS in passes of 8 output
+//     registers per lane (two passes at M > 16), which keeps the reduction
+//     buffer at 16 KB.
 //   * DUMP: each stage's exact partial group sums of rows [pm0, pm0 + pmr) are
 //     added with integer atomics into the zeroed P[pmr][N][K/G] (the sum over a
 //     group's stages is exact in any order); sa == nullptr skips the scales
@@ -58,6 +69,9 @@ constexpr int NWAVE = 8;
 constexpr int COLS = 32;
 constexpr int ROWS = 32;
 constexpr int MAX_SC_LDS = 60 * 1024;         // bytes of each staged scale block ([K/G][32] binary16)
+constexpr int RED_ROWS = 8;                    // output registers per lane reduced per pass
+constexpr int LDS_TOTAL = 160 * 1024;          // LDS per workgroup on gfx950
+constexpr int MAX_DYN_LDS = LDS_TOTAL - NWAVE * RED_ROWS * 64 * 4;   // scales (+ activations)
 constexpr int DECODE_PF = 6;                   // stages in flight per wave
 constexpr uint32_t MAGIC_BITS = 0x4B400000u;  // binary32 1.5 * 2^23
 constexpr float MAGIC = 12582912.0f;
@@ -80,7 +94,7 @@ __device__ __forceinline__ i32x4 frag2(uint32_t w0, uint32_t w1) {
 // rows 8 (r / 4) + 4 (l / 32) + r % 4 for r < MROWS / 2.
 // TAIL: K % 128 != 0, the last stage is partial and its loads are masked
 // (only then: the masks cost selects on every load).
-template <int MROWS, int PF, int GPS, bool DUMP, bool TAIL>
+template <int MROWS, int PF, int GPS, bool DUMP, bool TAIL, bool ALDS>
 __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, int G, uint16_t* __restrict__ Y,
@@ -88,9 +102,11 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     const bool have_sc = !DUMP || sa != nullptr;  // uniform
     const bool tiled = GPS == 1 && wt != 0;       // uniform
     constexpr int NR = MROWS / 2;      // output registers per lane that matter
-    __shared__ float red[NWAVE][NR][64];
+    constexpr int RR = NR < RED_ROWS ? NR : RED_ROWS;
+    __shared__ float red[NWAVE][RR][64];
     // [K/G][32] twice: activation scale of row r and group g at g * 32 + r, then
     // the weight scale of the current tile's column c and group g at g * 32 + c;
+    // then (ALDS) the packed activation rows 0 .. M-1 (swizzled 16-byte chunks)
     extern __shared__ uint16_t sas[];
 
     const int tid = threadIdx.x;
@@ -114,6 +130,9 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     // four per thread with every load issued before the LDS stores, so a staging
     // pass costs one load latency.
     uint16_t* wsc = sas + ng * ROWS;
+    // staged activation chunk c of row r sits at 16-byte place r * K/32 + (c ^ (r & 15))
+    // (K % 512 == 0), so the 16 rows of a fragment read hit 16 different bank groups
+    uint8_t* alds = reinterpret_cast<uint8_t*>(sas + 2 * ng * ROWS);
     constexpr int NT = 64 * NWAVE;
     // one or two [32][K/G] blocks (row r at base + min(r, rmax) * K/G) into LDS
     // group-major; a pass covers four 16-byte vectors per thread (two of each
@@ -211,7 +230,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 
     // ring of in-flight stages; (lt, li) is the next (tile, stage) to load.  No
     // load is issued past the last stage.
-    uint4 rw[PF][2], ra[PF][2];
+    uint4 rw[PF][2], ra[ALDS ? 1 : PF][2];
     int lt = 0, li = 0;
     // 32 packed bytes of one lane for a stage: two 16-byte runs (GPS == 1), or
     // four 8-byte pieces 16 apart (one per MFMA) when groups are finer than a stage
@@ -240,7 +259,8 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const uint8_t* ab = Aq + static_cast<int64_t>(s) * 64;
         const int lim = TAIL ? kb - s * 64 : 64;
         load32(wb + w_voff, rw[j], tiled ? 64 : lim, w_jstride);  // the tiled layout is zero padded
-        load32(ab + a_voff, ra[j], lim, 16);
+        if constexpr (!ALDS) load32(ab + a_voff, ra[j], lim, 16);
+        else (void)ab;
         if (++li == per_tile) {
             if (lt + 1 < my_tiles) {
                 li = 0;
@@ -262,6 +282,20 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
 #pragma unroll
         for (int j = 0; j < PF; ++j) load(j);
     }
+    // ALDS: the packed activation rows go straight into LDS (global_load_lds,
+    // 1 KB per wave instruction: 16 bytes per lane at consecutive places), in
+    // the swizzled order of alds_slot; the waits come with the scale staging's
+    const int cpr = kb / 16;  // 16-byte chunks per activation row
+    if constexpr (ALDS) {
+        const int nch = M * cpr;
+        for (int b = wave; b * 64 < nch; b += NWAVE) {  // wave-uniform
+            const int slot = min(b * 64 + lane, nch - 1);  // the last block's spare lanes repeat a chunk
+            const int r = slot / cpr, c = (slot - r * cpr) ^ (r & 15);
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(Aq + static_cast<int64_t>(r) * kb + 16 * c),
+                (__attribute__((address_space(3))) void*)(alds + b * 1024), 16, 0, 0);
+        }
+    }
     // activation scales of rows 0 .. 31 (rows past M clamped) and the first
     // tile's weight scales, their loads in flight together
     const int c0 = tile_col0(0);
@@ -270,7 +304,8 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         else stage(sa, M - 1, sas, nullptr, 0, nullptr);
         if (pf_sc && my_tiles > 1) prefetch_wscales(1);
     }
-    __syncthreads();  // activation scales and the first tile's weight scales staged
+    if constexpr (ALDS) __builtin_amdgcn_s_waitcnt(0);  // this wave's LDS loads have landed
+    __syncthreads();  // activation scales, the first tile's weight scales (and activations) staged
 
     int pi = 0;  // stage-in-tile of the next processed stage
     int pt = 0;  // tile of the next processed stage
@@ -279,10 +314,30 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const bool live = s_raw < nks;
         const int s = min(s_raw, nks - 1);
         i32x4 bw[4], af[4];
+        uint4 la[2];
+        if constexpr (ALDS) {
+            // this lane's 32 packed activation bytes of stage s (row min(l32, M - 1)):
+            // chunks 4s + 2h, 4s + 2h + 1 (one group per stage), or 8 bytes at
+            // offset 8h of chunks 4s .. 4s + 3 (finer groups)
+            const int r = min(l32, M - 1);
+            const uint8_t* row = alds + r * cpr * 16;
+            auto chunk = [&](int c) __attribute__((always_inline)) { return row + 16 * (c ^ (r & 15)); };
+            if constexpr (GPS == 1) {
+                la[0] = *reinterpret_cast<const uint4*>(chunk(4 * s + 2 * lh));
+                la[1] = *reinterpret_cast<const uint4*>(chunk(4 * s + 2 * lh + 1));
+            } else {
+                const uint2 q0 = *reinterpret_cast<const uint2*>(chunk(4 * s) + 8 * lh);
+                const uint2 q1 = *reinterpret_cast<const uint2*>(chunk(4 * s + 1) + 8 * lh);
+                const uint2 q2 = *reinterpret_cast<const uint2*>(chunk(4 * s + 2) + 8 * lh);
+                const uint2 q3 = *reinterpret_cast<const uint2*>(chunk(4 * s + 3) + 8 * lh);
+                la[0] = make_uint4(q0.x, q0.y, q1.x, q1.y);
+                la[1] = make_uint4(q2.x, q2.y, q3.x, q3.y);
+            }
+        }
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
             const uint4& v = rw[j][kk >> 1];
-            const uint4& u = ra[j][kk >> 1];
+            const uint4& u = ALDS ? la[kk >> 1] : ra[j][kk >> 1];
             bw[kk] = (kk & 1) ? frag2(v.z, v.w) : frag2(v.x, v.y);
             af[kk] = (kk & 1) ? frag2(u.z, u.w) : frag2(u.x, u.y);
         }
@@ -328,24 +383,27 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     // stage the next tile's weight scales (every wave is past tile t's stages
     // after the first barrier; the second publishes the new scales)
     auto finish_tile = [&](int t) {
-#pragma unroll
-        for (int r = 0; r < NR; ++r) red[wave][r][lane] = acc[r];
-        __syncthreads();
-        if (have_sc && t + 1 < my_tiles) {
-            if (pf_sc) store_wscales();
-            else stage_wscales(t + 1);
-        }
         const int n0 = tile_col0(t);
-        for (int o = tid; o < NR * 64; o += 64 * NWAVE) {
-            const int r = o >> 6, ln = o & 63;
-            float v = 0.f;
 #pragma unroll
-            for (int w = 0; w < NWAVE; ++w) v += red[w][r][ln];
-            const int row = 8 * (r >> 2) + 4 * (ln >> 5) + (r & 3);
-            const int col = n0 + (ln & 31);
-            if (have_sc && row < M && col < N) Y[static_cast<int64_t>(row) * N + col] = __half_as_ushort(__float2half_rn(v));
+        for (int r0 = 0; r0 < NR; r0 += RR) {
+#pragma unroll
+            for (int r = 0; r < RR; ++r) red[wave][r][lane] = acc[r0 + r];
+            __syncthreads();
+            if (r0 == 0 && have_sc && t + 1 < my_tiles) {
+                if (pf_sc) store_wscales();
+                else stage_wscales(t + 1);
+            }
+            for (int o = tid; o < RR * 64; o += 64 * NWAVE) {
+                const int r = r0 + (o >> 6), ln = o & 63;
+                float v = 0.f;
+#pragma unroll
+                for (int w = 0; w < NWAVE; ++w) v += red[w][r - r0][ln];
+                const int row = 8 * (r >> 2) + 4 * (ln >> 5) + (r & 3);
+                const int col = n0 + (ln & 31);
+                if (have_sc && row < M && col < N) Y[static_cast<int64_t>(row) * N + col] = __half_as_ushort(__float2half_rn(v));
+            }
+            __syncthreads();
         }
-        __syncthreads();
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[r] = 0.f;
     };
@@ -366,35 +424,52 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     }
 }
 
-template <int PF, int GPS, bool DUMP, bool TAIL>
-hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
-                            int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
+// Bytes of staged scales, and of staged activation rows (whole 1 KB blocks)
+// when they fit (ALDS; K % 512 == 0 for the swizzle, so never a partial stage).
+int64_t decode_scale_lds(int64_t K, int64_t G) { return 2 * (K / G) * ROWS * static_cast<int64_t>(sizeof(uint16_t)); }
+int64_t decode_a_lds(int64_t M, int64_t K) { return (M * (K / 2) + 1023) / 1024 * 1024; }
+bool decode_alds(int64_t M, int64_t K, int64_t G) {
+    return K % 512 == 0 && decode_a_lds(M, K) + decode_scale_lds(K, G) <= MAX_DYN_LDS;
+}
+
+template <int MROWS, int PF, int GPS, bool DUMP, bool TAIL, bool ALDS>
+hipError_t launch_decode_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                           int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
     static bool lds_attr_set = false;  // benign race: every caller sets the same value
+    const void* kern = reinterpret_cast<const void*>(w4a4_decode_kernel<MROWS, PF, GPS, DUMP, TAIL, ALDS>);
     if (!lds_attr_set) {
-        for (const void* k : {reinterpret_cast<const void*>(w4a4_decode_kernel<8, PF, GPS, DUMP, TAIL>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<16, PF, GPS, DUMP, TAIL>),
-                              reinterpret_cast<const void*>(w4a4_decode_kernel<32, PF, GPS, DUMP, TAIL>)}) {
-            const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * MAX_SC_LDS);
-            if (e != hipSuccess) return e;
-        }
+        const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, MAX_DYN_LDS);
+        if (e != hipSuccess) return e;
         lds_attr_set = true;
     }
     const int64_t tiles = (N + COLS - 1) / COLS;
     const int64_t grid = tiles < device_cu_count() ? tiles : device_cu_count();
-    const size_t lds = 2 * static_cast<size_t>(K / G) * ROWS * sizeof(uint16_t);
+    const size_t lds = static_cast<size_t>(decode_scale_lds(K, G) + (ALDS ? decode_a_lds(M, K) : 0));
     const dim3 gd(static_cast<unsigned>(grid)), bd(64 * NWAVE);
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), g = static_cast<int>(G);
-    const int w = wt ? 1 : 0;
-    if (M <= 8)
-        hipLaunchKernelGGL((w4a4_decode_kernel<8, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
-                           Y, dump.P, dump.m0, dump.mr, w);
-    else if (M <= 16)
-        hipLaunchKernelGGL((w4a4_decode_kernel<16, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
-                           Y, dump.P, dump.m0, dump.mr, w);
-    else
-        hipLaunchKernelGGL((w4a4_decode_kernel<32, PF, GPS, DUMP, TAIL>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n, k, g,
-                           Y, dump.P, dump.m0, dump.mr, w);
+    hipLaunchKernelGGL((w4a4_decode_kernel<MROWS, PF, GPS, DUMP, TAIL, ALDS>), gd, bd, lds, stream, Aq, sa, Wq, sw, m, n,
+                       k, g, Y, dump.P, dump.m0, dump.mr, wt ? 1 : 0);
     return hipGetLastError();
+}
+
+template <int PF, int GPS, bool DUMP, bool TAIL>
+hipError_t launch_decode_pf(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
+                            int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
+    // staging the activations costs one up-front read of them per workgroup,
+    // which pays once a wave walks at least 16 stages (several tiles or a long
+    // K); below that the per-stage loads overlap better (MI355X: N = K = 8192,
+    // one tile per workgroup, 3-9 % slower staged; 8-16 % faster at N = 28672
+    // and 57344)
+    const int64_t tiles = (N + COLS - 1) / COLS, cus = device_cu_count();
+    const int64_t wave_stages = (tiles + cus - 1) / cus * ((K / 128 + NWAVE - 1) / NWAVE);
+    const bool alds = !TAIL && wave_stages >= 16 && decode_alds(M, K, G);
+#define APEX4_DECODE_ROWS(R)                                                                                           \
+    return alds ? launch_decode_k<R, PF, GPS, DUMP, TAIL, !TAIL>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream)     \
+                : launch_decode_k<R, PF, GPS, DUMP, TAIL, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream)
+    if (M <= 8) APEX4_DECODE_ROWS(8);
+    if (M <= 16) APEX4_DECODE_ROWS(16);
+    APEX4_DECODE_ROWS(32);
+#undef APEX4_DECODE_ROWS
 }
 
 template <int PF, int GPS>

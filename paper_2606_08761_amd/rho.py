@@ -33,6 +33,8 @@ def _lib():
     L.apex4_rho_probe.restype = ctypes.c_int
     L.apex4_copy_probe.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
     L.apex4_copy_probe.restype = ctypes.c_int
+    L.apex4_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    L.apex4_read_probe.restype = ctypes.c_int
     L.apex4_rho_probe_ext.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int]
     L.apex4_rho_probe_ext.restype = ctypes.c_int
     L.apex4_rho_probe_issue.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int]
@@ -50,6 +52,21 @@ def copy(src, dst, stream=None):
                                  ctypes.c_void_p(stream.cuda_stream))
     if rc != 0:
         raise RuntimeError(f"apex4_copy_probe failed: {rc}")
+
+
+def read(src, sink, stream=None):
+    """Plain streaming read of all of `src` (a contiguous device tensor whose
+    byte size is a multiple of 16); `sink`: a device tensor of >= 4096 bytes."""
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(src.device)
+    if sink.numel() * sink.element_size() < 4096:
+        raise ValueError("sink must hold at least 4096 bytes")
+    nbytes = src.numel() * src.element_size()
+    rc = _lib().apex4_read_probe(ctypes.c_void_p(src.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                                 ctypes.c_void_p(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"apex4_read_probe failed: {rc}")
 
 
 def measure() -> dict:

@@ -333,3 +333,25 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros((4, 256), dtype=torch.float16)
     with pytest.raises(TypeError):
         pk.apex4_quantize_act(x, 128)
+
+
+def test_rho_library_exports_read_probe():
+    """The diagnostics library (ρ probes, the counter-calibration copy and the
+    streaming-read roofline) exports its entry points and validates arguments
+    before touching the GPU."""
+    import ctypes
+    from paper_2606_08761_amd import rho
+    if not os.path.exists(rho.LIB_PATH):
+        pytest.skip("librho_apex4.so not built")
+    L = rho._lib()
+    for name in ("apex4_rho_probe", "apex4_rho_probe_ext", "apex4_rho_probe_issue", "apex4_copy_probe",
+                 "apex4_read_probe"):
+        assert hasattr(L, name), name
+    buf = (ctypes.c_uint8 * 64)()
+    base = ctypes.addressof(buf)
+    aligned = (base + 15) & ~15
+    assert L.apex4_read_probe(None, 16, ctypes.c_void_p(aligned), None) == -1
+    assert L.apex4_read_probe(ctypes.c_void_p(aligned), 16, None, None) == -1
+    assert L.apex4_read_probe(ctypes.c_void_p(aligned), 15, ctypes.c_void_p(aligned), None) == -1
+    assert L.apex4_read_probe(ctypes.c_void_p(aligned + 1), 16, ctypes.c_void_p(aligned), None) == -1
+    assert L.apex4_read_probe(ctypes.c_void_p(aligned), 0, ctypes.c_void_p(aligned), None) == 0

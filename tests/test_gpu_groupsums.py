@@ -316,3 +316,38 @@ def test_decode_kernels_groupsums(O, M, N, K, G):
     P_o = O.groupsums(Aq, Wq, K, G)
     assert np.array_equal(host(P), P_o)
     assert np.array_equal(host(P2), P_o)
+
+
+# Shapes where the few-row kernel stages the activations in LDS (K % 512 == 0,
+# the M packed rows beside the scales within 144 KB, and each wave walking at
+# least 16 stages: ceil(tiles / CUs) * ceil(K / 1024) >= 16 on 256 CUs), at
+# every group kind: 32 and 64 (several groups per stage), 128, 256 (sums over
+# two stages), per channel, and an odd row count.
+DECODE_ALDS = [(4, 300, 32768, 64), (8, 9000, 8192, 32), (16, 600, 16384, 256), (32, 8300, 8192, 8192),
+               (3, 20000, 8192, 128), (32, 28672, 8192, 128)]
+
+
+@pytest.mark.parametrize("M,N,K,G", DECODE_ALDS)
+def test_decode_staged_activations(O, M, N, K, G):
+    import torch
+    m = pk()
+    tiles, stages = -(-N // 32), -(-K // 1024)
+    a_lds = -(-M * K // 2 // 1024) * 1024
+    assert K % 512 == 0 and a_lds + 2 * (K // G) * 64 <= 144 * 1024 and -(-tiles // 256) * stages >= 16
+    plan = m.apex4_w4a4_gemm_plan("gemm", M, N, K, G)
+    log(f"decode staged activations {M}x{N}x{K} G={G}: {plan}")
+    assert plan[0] == "decode"
+    r = np.random.default_rng(M * 7919 + N * 17 + K + G)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+    d = [dev(a) for a in (Aq, sa, Wq, sw)]
+    Y = m.apex4_w4a4_gemm(*d, G)
+    Yd, P = m.apex4_w4a4_gemm_debug(*d, G)
+    P2 = m.apex4_w4a4_gemm_groupsums(d[0], d[2], G)
+    Yt = m.apex4_w4a4_gemm_tiled(d[0], d[1], m.apex4_tile_weights(d[2]), d[3], G) if G >= 128 else Y
+    torch.cuda.synchronize()
+    assert torch.equal(Yd, Y) and torch.equal(Yt, Y)
+    P_o = O.groupsums(Aq, Wq, K, G)
+    assert np.array_equal(host(P), P_o)
+    assert np.array_equal(host(P2), P_o)
+    check_tolerance(host(Y), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"decode staged {M}x{N}x{K} G{G}")
