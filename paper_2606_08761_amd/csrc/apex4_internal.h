@@ -5,7 +5,23 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace apex4 {
+
+// Allows `bytes` of dynamic LDS for kernel k on the current device, once per
+// device: `done` (one per kernel, static at the call site) holds a bit per
+// device id below 64; a larger id sets the attribute on every call.
+inline hipError_t allow_dynamic_lds(const void* k, int bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = (dev >= 0 && dev < 64) ? (uint64_t{1} << dev) : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+    return e;
+}
 
 // Debug dump of the exact integer group sums P[m, n, g] (Eq. group_decomposition)
 // from the kernel that computes Y: rows [m0, m0 + mr) of the GEMM into

@@ -435,13 +435,10 @@ bool decode_alds(int64_t M, int64_t K, int64_t G) {
 template <int MROWS, int PF, int GPS, bool DUMP, bool TAIL, bool ALDS>
 hipError_t launch_decode_k(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                            int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream) {
-    static bool lds_attr_set = false;  // benign race: every caller sets the same value
-    const void* kern = reinterpret_cast<const void*>(w4a4_decode_kernel<MROWS, PF, GPS, DUMP, TAIL, ALDS>);
-    if (!lds_attr_set) {
-        const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, MAX_DYN_LDS);
-        if (e != hipSuccess) return e;
-        lds_attr_set = true;
-    }
+    static std::atomic<uint64_t> lds_allowed{0};
+    const hipError_t e = allow_dynamic_lds(
+        reinterpret_cast<const void*>(w4a4_decode_kernel<MROWS, PF, GPS, DUMP, TAIL, ALDS>), MAX_DYN_LDS, lds_allowed);
+    if (e != hipSuccess) return e;
     const int64_t tiles = (N + COLS - 1) / COLS;
     const int64_t grid = tiles < device_cu_count() ? tiles : device_cu_count();
     const size_t lds = static_cast<size_t>(decode_scale_lds(K, G) + (ALDS ? decode_a_lds(M, K) : 0));

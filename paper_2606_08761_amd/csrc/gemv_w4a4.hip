@@ -350,15 +350,11 @@ hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* W
         const size_t lds_t = gemv_tiled_lds_bytes(K, G);
         // above 64 KB of dynamic LDS the kernel must allow it (at most
         // 64 KB + K/2 <= 128 KB where gemv_fits holds and G >= 128)
-        static bool lds_attr_set = false;  // benign race: every caller sets the same value
-        if (!lds_attr_set) {
-            for (const void* kf : {reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, true>),
-                                   reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, false>)}) {
-                const hipError_t e = hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize, GT_MAX_LDS);
-                if (e != hipSuccess) return e;
-            }
-            lds_attr_set = true;
-        }
+        static std::atomic<uint64_t> lds_allowed[2] = {{0}, {0}};
+        const void* kf = dump.P ? reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, true>)
+                                : reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, false>);
+        const hipError_t ea = allow_dynamic_lds(kf, GT_MAX_LDS, lds_allowed[dump.P ? 1 : 0]);
+        if (ea != hipSuccess) return ea;
         if (lds_t > GT_MAX_LDS) return hipErrorInvalidValue;
         if (dump.P)
             hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, true>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, n, k, g,
