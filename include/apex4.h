@@ -209,9 +209,9 @@ int apex4_tile_weights(const uint8_t* W_q, int64_t N, int64_t K, uint8_t* W_t, v
  * G in {128, 256, 512, 1024} or G == K >= 128 (APEX4_ERR_GROUP otherwise: the
  * layout serves kernels that take one group per stage or more); W_t under
  * 4 GiB; other rules as apex4_w4a4_gemm.
- * With one row the result is within the tolerance of apex4_w4a4_gemm (the
- * one-row kernel adds its fp32 partial sums in another order) and otherwise
- * the same bits.
+ * With one or two rows the result is within the tolerance of
+ * apex4_w4a4_gemm (the dot-product kernel adds its fp32 partial sums in
+ * another order) and otherwise the same bits.
  */
 int apex4_w4a4_gemm_tiled(const uint8_t* A_q, const void* s_a,
                           const uint8_t* W_t, const void* s_w,

@@ -64,7 +64,7 @@ struct GemmPlan {
 };
 // split: the workspace path may split K; force_tile: no one-row, few-row or
 // ping-pong kernel (tests compare the general tile kernel against them).
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile);
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile, bool wt = false);
 
 // W4A4 GEMM: the one-row, few-row or tile kernel by shape (force_tile: always
 // the tile kernel, for tests).  With a dump, the same kernel also writes the
@@ -102,9 +102,9 @@ hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8
                               uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool wt = false);
 
 // W4A4 GEMM for one row on the vector ALUs (v_dot8_i32_i4 on the packed
-// codes): weight rows streamed from HBM in 1 KB runs.  gemv_fits() says
-// whether the shape is one it handles.
-bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G);
+// codes): weight rows streamed from HBM in 1 KB runs; two rows too on tiled
+// weights (wt).  gemv_fits() says whether the shape is one it handles.
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G, bool wt = false);
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                        int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump = Dump(),
                        bool wt = false);

@@ -406,7 +406,7 @@ int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, 
         return APEX4_OK;
     }
     const apex4::GemmPlan plan =
-        apex4::plan_gemm(M, N, K, G, entry == APEX4_ENTRY_GEMM_WS, (flags & APEX4_DEBUG_GENERAL_TILES) != 0);
+        apex4::plan_gemm(M, N, K, G, entry == APEX4_ENTRY_GEMM_WS, (flags & APEX4_DEBUG_GENERAL_TILES) != 0, wt);
     *kernel = plan.kernel;
     *splits = plan.splits;
     return APEX4_OK;

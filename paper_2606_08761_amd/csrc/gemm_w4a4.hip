@@ -1192,12 +1192,12 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream)
     return hipGetLastError();
 }
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool force_tile, bool wt) {
     if (split) {
         const int S = splitk_factor(M, N, K, G);
         if (S > 1) return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile64, S};
     }
-    if (!force_tile && gemv_fits(M, N, K, G)) return {kKernelGemv, 1};
+    if (!force_tile && gemv_fits(M, N, K, G, wt)) return {kKernelGemv, 1};
     if (!force_tile && decode_fits(M, N, K, G)) return {kKernelDecode, 1};
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (big_tiles < device_cu_count()) return {kKernelTile64, 1};
@@ -1226,7 +1226,7 @@ hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_
 hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
                               hipStream_t stream, Dump dump, bool force_tile, bool wt) {
-    const GemmPlan plan = plan_gemm(M, N, K, G, true, force_tile);
+    const GemmPlan plan = plan_gemm(M, N, K, G, true, force_tile, wt);
     if (plan.splits < 2) return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, nullptr, wt);
     const int S = plan.splits;
     // split ranges hold whole groups, so every group sum except the
@@ -1246,12 +1246,13 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
     return launch_splitk_reduce(part, S, M * N, Y, stream);
 }
 
-// One row: the dot-product kernel; up to 32 rows: the weight-streaming kernel;
-// otherwise the tile kernels (the same choice with or without a dump).
+// One row (two on tiled weights): the dot-product kernel; up to 32 rows: the
+// weight-streaming kernel; otherwise the tile kernels (the same choice with or
+// without a dump).
 hipError_t launch_gemm(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw,
                        int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump,
                        bool force_tile, bool wt) {
-    return launch_planned(plan_gemm(M, N, K, G, false, force_tile), Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump,
+    return launch_planned(plan_gemm(M, N, K, G, false, force_tile, wt), Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump,
                           nullptr, wt);
 }
 

@@ -32,9 +32,17 @@
 //     a workgroup takes one 32-row tile and its 8 waves split the tile's 1 KB
 //     runs; lanes l and l + 32 hold the same row, so a row's sum is one
 //     shuffle, then the waves' partials are added in a fixed order in LDS.
-//   * DUMP (pmr == 1): every lane's exact 32-code partial sum is added with an
-//     integer atomic into the zeroed P[1][N][K/G], giving the exact group sums
-//     whatever the order; sa == nullptr (codes only) skips the scales and Y.
+//   * Two rows (tiled weights, R = 2): every weight run is multiplied with
+//     both activation rows (both in LDS), so the weights are still read once;
+//     the VALU work doubles.  Measured on MI355X against the MFMA few-row
+//     kernel at M = 2 (tiled weights, rotated, graph replay): 7-12 % faster at
+//     N = 10240 and 28672 or K = 28672, even at N = K = 8192; at M = 3..4 the
+//     four-row form was 5-17 % slower and at M = 8 40-55 %, so only M = 2
+//     takes it.
+//   * DUMP (rows [pm0, pm0 + pmr) of the R): every lane's exact 32-code partial
+//     sum is added with an integer atomic into the zeroed P[pmr][N][K/G],
+//     giving the exact group sums whatever the order; sa == nullptr (codes
+//     only) skips the scales and Y.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -218,26 +226,30 @@ constexpr int GT_SWP = 16;                      // weight scales per thread load
 // a run lies in one group, g = 128 (q / 2) / G for every lane: the tile's
 // weight scales are staged in LDS group-major ([K/G][32], one coalesced pass)
 // and a run reads 32 consecutive ones.
-template <bool FUSE, int QL, bool DUMP>
+// R activation rows (1, or 2 without FUSE): A rows r at gv_lds + r K/32,
+// their scales at sa_lds + r K/G; rows past M repeat row M - 1 (never stored).
+template <bool FUSE, int QL, bool DUMP, int R = 1>
 __global__ __launch_bounds__(GT_NT) void w4a4_gemv_tiled_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wt,
-    const uint16_t* __restrict__ sw, int N, int K, int G, int lgG, uint16_t* __restrict__ Y,
+    const uint16_t* __restrict__ sw, int M, int N, int K, int G, int lgG, uint16_t* __restrict__ Y,
     const uint16_t* __restrict__ x, uint8_t* __restrict__ aq_out, uint16_t* __restrict__ sa_out,
-    int32_t* __restrict__ P, int pmr) {
+    int32_t* __restrict__ P, int pm0, int pmr) {
+    static_assert(R == 1 || !FUSE, "the fused prologue quantizes one row");
+    static_assert(R <= GT_WAVES, "one wave per output row in the final sum");
     const bool have_sc = FUSE || !DUMP || sa != nullptr;  // uniform
     extern __shared__ uint4 gv_lds[];
-    __shared__ float red[GT_WAVES][32];
+    __shared__ float red[GT_WAVES][R][32];
     const int tid = threadIdx.x, lane = tid & 63, lh = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int kb = K / 2;
+    const int kb = K / 2, kv = kb / 16;
     const int ng = K / G;
     const int nq = 2 * static_cast<int>(kstages(K));  // 1 KB runs per tile
     const int row = 32 * static_cast<int>(blockIdx.x) + (lane & 31);
     const bool row_ok = row < N;
     const int nmine = nq > wave ? (nq - wave + GT_WAVES - 1) / GT_WAVES : 0;  // runs of this wave (uniform)
     const uint8_t* wbase = Wt + static_cast<int64_t>(blockIdx.x) * nq * 1024 + 16 * lane;
-    float* sa_lds = reinterpret_cast<float*>(gv_lds + kb / 16);
-    uint16_t* sw_lds = reinterpret_cast<uint16_t*>(sa_lds + ng);  // [K/G][32]
+    float* sa_lds = reinterpret_cast<float*>(gv_lds + R * kv);
+    uint16_t* sw_lds = reinterpret_cast<uint16_t*>(sa_lds + R * ng);  // [K/G][32]
     // packed byte of A matching the lane's 16 weight bytes in run q
     auto a_off = [&](int q) { return 64 * (q >> 1) + 32 * lh + 16 * (q & 1); };
 
@@ -266,7 +278,19 @@ __global__ __launch_bounds__(GT_NT) void w4a4_gemv_tiled_kernel(
     uint16_t swv[GT_SWP];
 #pragma unroll
     for (int u = 0; u < GT_SWP; ++u) swv[u] = tid + u * GT_NT < nsw ? sw_at(tid + u * GT_NT) : static_cast<uint16_t>(0);
-    gv_stage_a<FUSE, QL, GT_NT>(gv_lds, sa_lds, Aq, sa, have_sc, K, ng, x, aq_out, sa_out);
+    if constexpr (R == 1) {
+        gv_stage_a<FUSE, QL, GT_NT>(gv_lds, sa_lds, Aq, sa, have_sc, K, ng, x, aq_out, sa_out);
+    } else {
+        for (int i = tid; i < R * kv; i += GT_NT) {
+            const int r = i / kv, c = i - r * kv;
+            gv_lds[i] = reinterpret_cast<const uint4*>(Aq + static_cast<int64_t>(min(r, M - 1)) * kb)[c];
+        }
+        if (have_sc)
+            for (int i = tid; i < R * ng; i += GT_NT) {
+                const int r = i / ng, g = i - r * ng;
+                sa_lds[i] = gv_h2f(sa[static_cast<int64_t>(min(r, M - 1)) * ng + g]);
+            }
+    }
 #pragma unroll
     for (int u = 0; u < GT_SWP; ++u) {
         const int i = tid + u * GT_NT;
@@ -275,7 +299,9 @@ __global__ __launch_bounds__(GT_NT) void w4a4_gemv_tiled_kernel(
     for (int i = tid + GT_SWP * GT_NT; i < nsw; i += GT_NT) sw_lds[(i % ng) * 32 + i / ng] = sw_at(i);
     __syncthreads();
 
-    float acc = 0.f;
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
     for (int i0 = 0; i0 < nmine; i0 += GV_LOADS) {
         if (i0 > 0) issue(i0);
 #pragma unroll
@@ -283,37 +309,47 @@ __global__ __launch_bounds__(GT_NT) void w4a4_gemv_tiled_kernel(
             if (i0 + j < nmine) {  // uniform
                 const int off = a_off(wave + (i0 + j) * GT_WAVES);
                 if (off < kb) {
-                    const uint4 a = gv_lds[off >> 4];
-                    int p = __builtin_amdgcn_sdot8(static_cast<int>(a.x), static_cast<int>(w[j].x), 0, false);
-                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.y), static_cast<int>(w[j].y), p, false);
-                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.z), static_cast<int>(w[j].z), p, false);
-                    p = __builtin_amdgcn_sdot8(static_cast<int>(a.w), static_cast<int>(w[j].w), p, false);
-                    if constexpr (DUMP) {
-                        if (pmr > 0 && row_ok) atomicAdd(&P[static_cast<int64_t>(row) * ng + ((2 * off) >> lgG)], p);
-                    }
-                    if (have_sc) {
-                        const int g = (2 * off) >> lgG;
-                        const float t = static_cast<float>(p) * sa_lds[g];
-                        acc = fmaf(t, gv_h2f(sw_lds[g * 32 + (lane & 31)]), acc);
+                    const int g = (2 * off) >> lgG;
+#pragma unroll
+                    for (int r = 0; r < R; ++r) {
+                        const uint4 a = gv_lds[r * kv + (off >> 4)];
+                        int p = __builtin_amdgcn_sdot8(static_cast<int>(a.x), static_cast<int>(w[j].x), 0, false);
+                        p = __builtin_amdgcn_sdot8(static_cast<int>(a.y), static_cast<int>(w[j].y), p, false);
+                        p = __builtin_amdgcn_sdot8(static_cast<int>(a.z), static_cast<int>(w[j].z), p, false);
+                        p = __builtin_amdgcn_sdot8(static_cast<int>(a.w), static_cast<int>(w[j].w), p, false);
+                        if constexpr (DUMP) {
+                            if (row_ok && r >= pm0 && r < pm0 + pmr)
+                                atomicAdd(&P[(static_cast<int64_t>(r - pm0) * N + row) * ng + g], p);
+                        }
+                        if (have_sc) {
+                            const float t = static_cast<float>(p) * sa_lds[r * ng + g];
+                            acc[r] = fmaf(t, gv_h2f(sw_lds[g * 32 + (lane & 31)]), acc[r]);
+                        }
                     }
                 }
             }
         }
     }
-    acc += __shfl_xor(acc, 32, 64);  // the row's two lane halves
-    if (lane < 32) red[wave][lane] = acc;
-    __syncthreads();
-    if (wave == 0 && lane < 32 && have_sc && row_ok) {
-        float v = red[0][lane];
 #pragma unroll
-        for (int u = 1; u < GT_WAVES; ++u) v += red[u][lane];
-        Y[row] = __half_as_ushort(__float2half_rn(v));
+    for (int r = 0; r < R; ++r) {
+        acc[r] += __shfl_xor(acc[r], 32, 64);  // the row's two lane halves
+        if (lane < 32) red[wave][r][lane] = acc[r];
+    }
+    __syncthreads();
+    // wave r adds row r's eight wave partials in wave order
+    if (wave < R && wave < M && lane < 32 && have_sc && row_ok) {
+        float v = red[0][wave][lane];
+#pragma unroll
+        for (int u = 1; u < GT_WAVES; ++u) v += red[u][wave][lane];
+        Y[static_cast<int64_t>(wave) * N + row] = __half_as_ushort(__float2half_rn(v));
     }
 }
 
 size_t gemv_lds_bytes(int64_t K, int64_t G) { return static_cast<size_t>(K / 2) + 4 * static_cast<size_t>(K / G); }
-// tiled: plus the tile's weight scales, binary16 [K/G][32]
-size_t gemv_tiled_lds_bytes(int64_t K, int64_t G) { return gemv_lds_bytes(K, G) + 64 * static_cast<size_t>(K / G); }
+// tiled, R rows: R rows of codes and scales plus the tile's weight scales, binary16 [K/G][32]
+size_t gemv_tiled_lds_bytes(int64_t K, int64_t G, int R = 1) {
+    return R * gemv_lds_bytes(K, G) + 64 * static_cast<size_t>(K / G);
+}
 
 // Rows per wave and workgroups: fill the load batch, but keep at least 8 waves
 // per CU when N allows.
@@ -330,10 +366,10 @@ GemvGrid gemv_grid(int64_t N, int64_t K) {
     return {rpw, (waves + GV_WAVES - 1) / GV_WAVES};
 }
 
-template <bool FUSE, int QL>
+template <bool FUSE, int QL, int R = 1>
 hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t N,
                          int64_t K, int64_t G, uint16_t* Y, const uint16_t* x, uint8_t* aq_out, uint16_t* sa_out,
-                         Dump dump, bool wt, hipStream_t stream) {
+                         Dump dump, bool wt, hipStream_t stream, int64_t M = 1) {
     int lgG = 31;
     if (G != K)
         for (lgG = 5; (int64_t{1} << lgG) < G; ++lgG) {
@@ -347,23 +383,25 @@ hipError_t launch_gemv_t(const uint8_t* Aq, const uint16_t* sa, const uint8_t* W
     }
     if (wt) {
         const dim3 gd(static_cast<unsigned>((N + 31) / 32)), bd(GT_NT);
-        const size_t lds_t = gemv_tiled_lds_bytes(K, G);
+        const size_t lds_t = gemv_tiled_lds_bytes(K, G, R);
         // above 64 KB of dynamic LDS the kernel must allow it (at most
-        // 64 KB + K/2 <= 128 KB where gemv_fits holds and G >= 128)
+        // GT_MAX_LDS where the fits functions hold)
         static std::atomic<uint64_t> lds_allowed[2] = {{0}, {0}};
-        const void* kf = dump.P ? reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, true>)
-                                : reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, false>);
+        const void* kf = dump.P ? reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, true, R>)
+                                : reinterpret_cast<const void*>(w4a4_gemv_tiled_kernel<FUSE, QL, false, R>);
         const hipError_t ea = allow_dynamic_lds(kf, GT_MAX_LDS, lds_allowed[dump.P ? 1 : 0]);
         if (ea != hipSuccess) return ea;
         if (lds_t > GT_MAX_LDS) return hipErrorInvalidValue;
+        const int m = static_cast<int>(M);
         if (dump.P)
-            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, true>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, n, k, g,
-                               lgG, Y, x, aq_out, sa_out, dump.P, dump.mr);
+            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, true, R>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, m, n,
+                               k, g, lgG, Y, x, aq_out, sa_out, dump.P, dump.m0, dump.mr);
         else
-            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, false>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, n, k, g,
-                               lgG, Y, x, aq_out, sa_out, static_cast<int32_t*>(nullptr), 0);
+            hipLaunchKernelGGL((w4a4_gemv_tiled_kernel<FUSE, QL, false, R>), gd, bd, lds_t, stream, Aq, sa, Wq, sw, m,
+                               n, k, g, lgG, Y, x, aq_out, sa_out, static_cast<int32_t*>(nullptr), 0, 0);
         return hipGetLastError();
     }
+    if constexpr (R != 1) return hipErrorInvalidValue;  // several rows: tiled weights only
     const GemvGrid gg = gemv_grid(N, K);
     const dim3 gd(static_cast<unsigned>(gg.grid)), bd(GV_NT);
     const int rpw = static_cast<int>(gg.rpw);
@@ -381,14 +419,18 @@ int64_t gemv_workgroups(int64_t N, int64_t K, bool wt) { return wt ? (N + 31) / 
 
 }  // namespace
 
-bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G) {
+bool gemv_fits(int64_t M, int64_t N, int64_t K, int64_t G, bool wt) {
     const bool g_ok = G == K || G == 32 || G == 64 || G == 128 || G == 256 || G == 512 || G == 1024;
+    if (M == 2)  // two rows: tiled weights (G >= 128), both rows in LDS
+        return wt && N >= 1 && g_ok && G >= 128 && gemv_tiled_lds_bytes(K, G, 2) <= GT_MAX_LDS;
     return M == 1 && N >= 1 && g_ok && gemv_lds_bytes(K, G) <= GV_MAX_LDS;
 }
 
 hipError_t launch_gemv(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                        int64_t N, int64_t K, int64_t G, uint16_t* Y, hipStream_t stream, Dump dump, bool wt) {
-    if (!gemv_fits(M, N, K, G) || (wt && G < 128)) return hipErrorInvalidValue;
+    if (!gemv_fits(M, N, K, G, wt) || (wt && G < 128)) return hipErrorInvalidValue;
+    if (M == 2)
+        return launch_gemv_t<false, 1, 2>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, dump, wt, stream, M);
     return launch_gemv_t<false, 1>(Aq, sa, Wq, sw, N, K, G, Y, nullptr, nullptr, nullptr, dump, wt, stream);
 }
 
@@ -403,7 +445,7 @@ constexpr int64_t GV_FUSE_WORK = int64_t{1} << 23;
 constexpr int64_t GT_FUSE_WORK = int64_t{1} << 21;
 
 bool fused_linear_fits(int64_t M, int64_t N, int64_t K, int64_t G, bool wt) {
-    return gemv_fits(M, N, K, G) && (G == 32 || G == 64 || G == 128 || G == 256 || G == 512) && G < K &&
+    return M == 1 && gemv_fits(M, N, K, G) && (G == 32 || G == 64 || G == 128 || G == 256 || G == 512) && G < K &&
            !(wt && G < 128) && gemv_workgroups(N, K, wt) * K <= (wt ? GT_FUSE_WORK : GV_FUSE_WORK);
 }
 

@@ -6,8 +6,8 @@ entry points that read it.
     zero past N and K/2 (ragged N and K included);
   * Y from tiled weights equals Y from row-major weights bit for bit on every
     kernel that reads the same lane fragments (streaming, both tile kernels,
-    ping-pong, split over K), and is within tolerance of the oracle on one row
-    (that kernel adds its partial sums in another order);
+    ping-pong, split over K), and is within tolerance of the oracle on one or
+    two rows (the dot-product kernel adds its partial sums in another order);
   * exact group sums through the tiled paths (debug dump) against the oracle;
   * the linear entry point: Y and work buffers equal quantize-then-GEMM.
 """
@@ -87,7 +87,11 @@ def test_tiled_gemm_equals_row_major(O, M, N, K, G):
     m0, mr = (0, M) if M <= 64 else (M - 40, 36)
     Yd, P = m.apex4_w4a4_gemm_debug(a, s1, wt, s2, G, m0, mr, flags=m.APEX4_DEBUG_W_TILED)
     torch.cuda.synchronize()
-    assert torch.equal(Yt, Y)
+    if plan[0] == "gemv":  # two rows on tiled weights: the dot-product kernel
+        assert M == 2
+        check_tolerance(host(Yt), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"tiled two rows N={N} K={K} G={G}")
+    else:
+        assert torch.equal(Yt, Y)
     assert torch.equal(Yd, Yt)
     assert np.array_equal(host(P), O.groupsums(Aq, Wq, K, G, m0, mr))
 
@@ -148,6 +152,46 @@ def test_tiled_one_row(O, M, N, K, G):
     P_o = O.groupsums(Aq_o, Wq_o, K, G)
     assert np.array_equal(host(P), P_o) and np.array_equal(host(Pl), P_o)
     check_tolerance(host(Y), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"tiled one row N={N} K={K} G={G}")
+
+
+# two rows: the two-row form of the tiled dot-product kernel (ragged N, K past
+# 64 KB of codes per row, G > 128 with sub-group partials, per channel)
+TWO_ROWS = [(2, 8192, 8192, 128), (2, 28672, 8192, 128), (2, 10240, 8192, 128), (2, 8192, 28672, 128),
+            (2, 1000, 4096, 256), (2, 257, 2048, 1024), (2, 300, 3072, 3072), (2, 33, 8224, 8224),
+            (2, 520, 8192, 512), (2, 100, 57344, 128)]
+
+
+@pytest.mark.parametrize("M,N,K,G", TWO_ROWS)
+def test_tiled_two_rows(O, M, N, K, G):
+    import torch
+    m = pk()
+    T = m.APEX4_DEBUG_W_TILED
+    plans = (m.apex4_w4a4_gemm_plan("gemm", M, N, K, G, T), m.apex4_w4a4_gemm_plan("linear", M, N, K, G, T),
+             m.apex4_w4a4_gemm_plan("gemm", M, N, K, G))
+    log(f"tiled two rows N={N} K={K} G={G}: gemm {plans[0]}, linear {plans[1]}, row-major {plans[2]}")
+    assert plans[0] == ("gemv", 1) and plans[1] == ("gemv", 1) and plans[2] == ("decode", 1)
+    w = wl.weights(wl.rng_for("decode", 17, N + K), N, K)
+    x = wl.activations(wl.rng_for("decode", 18, K + G), M, K)
+    Wq_d, sw_d = m.apex4_quantize_act(dev(w), G)
+    Wt = m.apex4_tile_weights(Wq_d)
+    Aq_d, sa_d = m.apex4_quantize_act(dev(x), G)
+    Y = m.apex4_w4a4_gemm_tiled(Aq_d, sa_d, Wt, sw_d, G)
+    Aw = torch.full((M, K // 2), 0xAB, dtype=torch.uint8, device="cuda")
+    saw = torch.full((M, K // G), float("nan"), dtype=torch.float16, device="cuda")
+    Yl = m.apex4_w4a4_linear_tiled(dev(x), Wt, sw_d, G, A_q_work=Aw, s_a_work=saw)
+    dumps = [m.apex4_w4a4_gemm_debug(Aq_d, sa_d, Wt, sw_d, G, m0, mr, flags=T) for m0, mr in ((0, 2), (1, 1), (0, 1))]
+    Yld, _, _, Pl = m.apex4_w4a4_linear_debug(dev(x), Wt, sw_d, G, flags=T)
+    torch.cuda.synchronize()
+    assert torch.equal(Aw, Aq_d) and torch.equal(saw.view(torch.int16), sa_d.view(torch.int16))
+    assert torch.equal(Yl, Y) and torch.equal(Yld, Y) and all(torch.equal(Yd, Y) for Yd, _ in dumps)
+    Wq_o, sw_o = O.quantize(w, G)
+    Aq_o, sa_o = O.quantize(x, G)
+    assert np.array_equal(host(Wq_d), Wq_o) and np.array_equal(host(Aq_d), Aq_o)
+    P_o = O.groupsums(Aq_o, Wq_o, K, G)
+    assert np.array_equal(host(Pl), P_o)
+    for (m0, mr), (_, P) in zip(((0, 2), (1, 1), (0, 1)), dumps):
+        assert np.array_equal(host(P), P_o[m0:m0 + mr]), (m0, mr)
+    check_tolerance(host(Y), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"tiled two rows N={N} K={K} G={G}")
 
 
 @pytest.mark.parametrize("M", [5, 32, 300])
