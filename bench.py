@@ -368,7 +368,11 @@ def layers_mode(reps: int = 10):
                     def call(i):
                         linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa)
                 t = graph_timed(call, reps)
-                split[name] = need // (4 * Ml * Nl) if need else 1
+                # the workspace's use: S K ranges on the tile kernels, or the
+                # stream-K form of the few-row kernel (reported as 0)
+                kern_ws, s_ws = pk.apex4_w4a4_gemm_plan("gemm_ws", Ml, Nl, Kl, Gv,
+                                                        pk.APEX4_DEBUG_W_TILED if tiled else 0)
+                split[name] = 0 if kern_ws == "decode_split" else (s_ws if need else 1)
                 per[name] = round(t, 2)
                 # algorithmic HBM bytes of the linear: x, codes, scales, Y
                 nbytes = 2 * Ml * Kl + Ml * Kl / 2 + Nl * Kl / 2 + 2 * (Ml + Nl) * Kl / Gv + 2 * Ml * Nl
@@ -433,7 +437,8 @@ def summarize_layers(path, command):
              "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
              "Each W4A4 linear is timed as W4A4Linear runs it: quantize + GEMM from fp16 activations "
              "(apex4_w4a4_linear_tiled on tiled weights for G >= 128, apex4_w4a4_linear on row-major weights "
-             "below; or the quantizer + the GEMM split over K into S ranges with a workspace, marked S=) "
+             "below; or, where the library asks for a workspace, the quantizer + the GEMM with it: split over K into S "
+             "ranges on the tile kernels, marked S=, or the few-row kernel's stream-K form, marked stream-K) "
              "from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
              "torch.matmul (hipBLASLt) on the same shapes, rotated the same way, timed eagerly. "
              "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
@@ -463,7 +468,8 @@ def summarize_layers(path, command):
         g, sp = r.get("hbm_gbs", {}), r.get("k_splits", {})
         lines.append(f"| {r['config']} | {r['M']} | " +
                      ", ".join(f"{k} {v}" + (f" ({g[k]} GB/s)" if k in g else "") +
-                               (f" S={sp[k]}" if sp.get(k, 1) > 1 else "") for k, v in r["linear_us"].items()) + " |")
+                               (f" S={sp[k]}" if sp.get(k, 1) > 1 else "") +
+                               (" stream-K" if sp.get(k, 1) == 0 else "") for k, v in r["linear_us"].items()) + " |")
     with open(os.path.join(ROOT, "profiles", "layer_sweep_llama2_70b.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 

@@ -170,6 +170,7 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
 #define APEX4_KERNEL_TILE_64 4    /* 64 x 128 output tiles */
 #define APEX4_KERNEL_TILE_128 5   /* 128 x 256 output tiles */
 #define APEX4_KERNEL_PINGPONG 6   /* G = 128 on 128 x 256 tiles, MFMA and dequant waves alternating */
+#define APEX4_KERNEL_DECODE_SPLIT 7 /* up to 32 rows, stream-K over the CUs (workspace entry points) */
 
 /*
  * The GEMM kernel that `entry` runs for this shape on the current device, and
@@ -262,12 +263,22 @@ int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w,
  * compute units (M > 32), K is split into S in {2, 4, 8} ranges of whole
  * groups; each workgroup writes a partial tile into the workspace (fp32, or
  * the exact int32 sums for G == K), and a second kernel sums the S partials in
- * range order and rounds once to binary16.  Y is then within the tolerance of
- * apex4_w4a4_gemm (the fp32 summation order differs; for G == K it is the same
- * bits), deterministic for a given shape and device.
+ * range order and rounds once to binary16.  With M <= 32 rows, where the
+ * 32-column tiles leave more than a tenth of the compute units idle in the last
+ * round and the tiles are long (at least 128 stage-groups, i.e. K/128 stages
+ * times 128/G groups per stage, below one tile per compute unit; K >= 24576
+ * above), the few-row kernel runs in a stream-K form: the full rounds stay
+ * whole tiles, the remaining tiles' 128-wide K stages are spread evenly over
+ * the workgroups, and a tile cut between workgroups has its fp32 parts added in
+ * segment order by the workgroup that finishes last (counters cleared by a
+ * kernel on every call, so a captured call replays).  Y is then within the
+ * tolerance of apex4_w4a4_gemm (the fp32 summation order differs; for G == K
+ * the tile kernels' split gives the same bits), deterministic for a given shape
+ * and device.
  *
  * apex4_w4a4_gemm_workspace_size writes to *bytes the workspace this shape
- * needs on the current device: S * M * N * 4, or 0 where no split applies (then
+ * needs on the current device: S * M * N * 4 for the split over K, counters
+ * and fp32 parts for the stream-K form, or 0 where neither applies (then
  * apex4_w4a4_gemm_ws is apex4_w4a4_gemm and workspace may be NULL).
  *
  *   workspace: caller-owned device memory, 16-byte aligned, at least *bytes

@@ -27,7 +27,8 @@ APEX4_DEBUG_GENERAL_TILES = 1
 APEX4_DEBUG_W_TILED = 2
 APEX4_NOALLOC_SCRATCH_BYTES = 32 << 20
 ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2}
-KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong"}
+KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong",
+           7: "decode_split"}
 
 EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums", "apex4_w4a4_gemm_debug",
             "apex4_w4a4_gemm_plan", "apex4_w4a4_linear", "apex4_w4a4_linear_debug", "apex4_pack_fp6",

@@ -57,10 +57,11 @@ enum GemmKernel : int {
     kKernelTile64 = 4,    // 64 x 128 tiles, 4 waves (K may split inside the workgroup)
     kKernelTile128 = 5,   // 128 x 256 tiles, 8 waves
     kKernelPingPong = 6,  // G = 128 on 128 x 256 tiles, ping-pong schedule
+    kKernelDecodeSplit = 7,  // the few-row kernel in stream-K form (workspace path)
 };
 struct GemmPlan {
     GemmKernel kernel;
-    int splits;  // S > 1: split over K across workgroups (workspace path)
+    int splits;  // S > 1: split over K across workgroups (workspace path; tile kernels)
 };
 // split: the workspace path may split K; force_tile: no one-row, few-row or
 // ping-pong kernel (tests compare the general tile kernel against them).
@@ -97,9 +98,16 @@ int device_cu_count();
 // W4A4 GEMM for few rows: weights streamed once, K split over the waves of a
 // workgroup.  decode_fits() says whether the shape is one it handles.
 bool decode_fits(int64_t M, int64_t N, int64_t K, int64_t G);
+// workspace (decode_split_workspace_bytes(M, N, K, G) bytes, or nullptr): when
+// the round-robin tiles leave CUs idle, the stream-K form of the kernel evens
+// the (tile, stage) units out over the CUs and adds the parts of cut tiles
+// through the workspace in a fixed order (decode_split_workspace_bytes is 0
+// where it does not apply).
+int64_t decode_split_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G);
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq,
                               const uint16_t* sw, int64_t M, int64_t N, int64_t K, int64_t G,
-                              uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool wt = false);
+                              uint16_t* Y, hipStream_t stream, Dump dump = Dump(), bool wt = false,
+                              void* workspace = nullptr);
 
 // W4A4 GEMM for one row on the vector ALUs (v_dot8_i32_i4 on the packed
 // codes): weight rows streamed from HBM in 1 KB runs; two rows too on tiled

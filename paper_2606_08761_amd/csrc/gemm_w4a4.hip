@@ -1172,6 +1172,8 @@ int splitk_factor(int64_t M, int64_t N, int64_t K, int64_t G) {
 }
 
 int64_t splitk_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t G) {
+    // few rows: the stream-K form of the few-row kernel where it applies
+    if (M > 0 && !gemv_fits(M, N, K, G) && decode_fits(M, N, K, G)) return decode_split_workspace_bytes(M, N, K, G);
     const int S = splitk_factor(M, N, K, G);
     return S > 1 ? static_cast<int64_t>(S) * M * N * 4 : 0;
 }
@@ -1198,7 +1200,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool 
         if (S > 1) return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile64, S};
     }
     if (!force_tile && gemv_fits(M, N, K, G, wt)) return {kKernelGemv, 1};
-    if (!force_tile && decode_fits(M, N, K, G)) return {kKernelDecode, 1};
+    if (!force_tile && decode_fits(M, N, K, G))
+        return {split && decode_split_workspace_bytes(M, N, K, G) > 0 ? kKernelDecodeSplit : kKernelDecode, 1};
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (big_tiles < device_cu_count()) return {kKernelTile64, 1};
     return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile128, 1};
@@ -1212,6 +1215,7 @@ hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_
     switch (plan.kernel) {
         case kKernelGemv: return launch_gemv(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, wt);
         case kKernelDecode: return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, wt);
+        case kKernelDecodeSplit: return launch_gemm_decode(Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, wt, part);
         case kKernelTile64:
             return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, plan.splits, part);
         case kKernelTile128:
@@ -1227,6 +1231,8 @@ hipError_t launch_gemm_splitk(const uint8_t* Aq, const uint16_t* sa, const uint8
                               int64_t M, int64_t N, int64_t K, int64_t G, uint16_t* Y, float* part,
                               hipStream_t stream, Dump dump, bool force_tile, bool wt) {
     const GemmPlan plan = plan_gemm(M, N, K, G, true, force_tile, wt);
+    if (plan.kernel == kKernelDecodeSplit)  // the workspace holds the stream-K counters and parts
+        return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, part, wt);
     if (plan.splits < 2) return launch_planned(plan, Aq, sa, Wq, sw, M, N, K, G, Y, stream, dump, nullptr, wt);
     const int S = plan.splits;
     // split ranges hold whole groups, so every group sum except the

@@ -228,8 +228,8 @@ def test_llama70b_linear_groupsums(O, linear):
         x = wl.activations(wl.rng_for("llama70b", 20, M * 100 + K // 1024), M, K)
         lin, ws = _linear_case(O, f"{linear} M={M}", W, x, G, M)
         kernels.update((lin[0], ws[0]))
-        if M == 16:
-            assert lin == ("decode", 1) and ws == ("decode", 1)
+        if M == 16:  # the workspace entry takes the stream-K form where round robin leaves CUs idle
+            assert lin == ("decode", 1) and ws in (("decode", 1), ("decode_split", 1))
         if M == 4096:
             assert lin == ("pingpong", 1)
     log(f"llama70b {linear}: kernels {sorted(kernels)}")
