@@ -48,7 +48,7 @@ def parse():
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
     p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers", "variants",
-                                      "decode_counters"),
+                                      "decode_counters", "decode_split"),
                    default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
@@ -279,6 +279,100 @@ MX_LAYER_CONFIGS = {
     "mx_g32": [(n, N_, K_, 32) for n, N_, K_, _ in LAYER_CONFIGS["g128"]],
     "mx_g128": [(n, N_, K_, 128) for n, N_, K_, _ in LAYER_CONFIGS["g128"]],
 }
+
+
+def decode_split_mode(reps: int = 40, rounds: int = 6):
+    """The few-row GEMM with and without a workspace (round robin against the
+    stream-K form where the plan takes it), over N x K x G x M; graph replay of
+    `reps` calls, the two forms alternated `rounds` times (median), weights
+    rotated past the Infinity Cache.  Writes profiles/decode_stream_k.md."""
+    import statistics
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def capture(fn):
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for i in range(reps):
+                fn(i)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        return g
+
+    def once(g):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    rows = []
+    for G in (32, 128):
+        for K in (8192, 28672):
+            for N in (64, 256, 1024, 2048, 4096, 8192, 10240):
+                for M in (4, 16):
+                    tiled = G >= 128
+                    kern, _ = pk.apex4_w4a4_gemm_plan("gemm_ws", M, N, K, G, pk.APEX4_DEBUG_W_TILED if tiled else 0)
+                    need = pk.apex4_w4a4_gemm_workspace_size(M, N, K, G)
+                    r = wl.rng_for("decode", 7, M * 100003 + N * 7 + K + G)
+                    Wq = torch.from_numpy(wl.random_codes(r, N, K)).to(dev)
+                    W = pk.apex4_tile_weights(Wq) if tiled else Wq
+                    sw = torch.from_numpy(wl.random_scales(r, N, K // G)).to(dev)
+                    R = max(2, -(-ROTATE_BYTES // W.numel()))
+                    wset = [W.clone() for _ in range(R)]
+                    x = torch.from_numpy(wl.activations(r, M, K)).to(dev)
+                    Aq, sa = pk.apex4_quantize_act(x, G)
+                    work = torch.empty((max(need, 16),), dtype=torch.uint8, device=dev)
+                    Y0 = torch.empty((M, N), dtype=torch.float16, device=dev)
+                    Y1 = torch.empty_like(Y0)
+                    if tiled:
+                        def f0(i):
+                            pk.apex4_w4a4_gemm_tiled(Aq, sa, wset[i % R], sw, G, None, Y0)
+
+                        def f1(i):
+                            pk.apex4_w4a4_gemm_tiled(Aq, sa, wset[i % R], sw, G, work, Y1)
+                    else:
+                        def f0(i):
+                            pk.apex4_w4a4_gemm(Aq, sa, wset[i % R], sw, G, Y0)
+
+                        def f1(i):
+                            pk.apex4_w4a4_gemm_ws(Aq, sa, wset[i % R], sw, G, work, Y1)
+                    g0, g1 = capture(f0), capture(f1)
+                    t0, t1 = [], []
+                    for _ in range(rounds):
+                        t0.append(once(g0))
+                        t1.append(once(g1))
+                    del g0, g1, wset, W, Wq
+                    a, b = statistics.median(t0), statistics.median(t1)
+                    row = {"mode": "decode_split", "M": M, "N": N, "K": K, "G": G, "plan_ws": kern,
+                           "workspace_bytes": need, "round_robin_us": round(a, 2), "workspace_us": round(b, 2),
+                           "ratio": round(b / a, 3)}
+                    rows.append(row)
+                    print(json.dumps(row), flush=True)
+    lines = ["# Few-row GEMM: round robin against the stream-K form", "",
+             "Command (run from the repository root on one MI355X):", "", "```",
+             "python3 bench.py --mode decode_split", "```", "",
+             f"Each shape: {reps} calls captured in a graph per form, the two graphs replayed alternately "
+             f"{rounds} times (median per call), weights rotated over >= {ROTATE_BYTES >> 20} MB of copies, "
+             "random codes and scales. Round robin: the entry without a workspace (apex4_w4a4_gemm_tiled for "
+             "G = 128 on tiled weights, apex4_w4a4_gemm for G = 32). Workspace: the same entry with the workspace "
+             "the size query returns; it runs the stream-K form where the plan says decode_split, otherwise the "
+             "same kernel as round robin (ratio ~1 there is the run-to-run spread).", "",
+             "| G | K | N | M | plan (workspace entry) | workspace bytes | round robin µs | workspace µs | ratio |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r_ in rows:
+        lines.append(f"| {r_['G']} | {r_['K']} | {r_['N']} | {r_['M']} | {r_['plan_ws']} | {r_['workspace_bytes']} | "
+                     f"{r_['round_robin_us']} | {r_['workspace_us']} | {r_['ratio']} |")
+    with open(os.path.join(ROOT, "profiles", "decode_stream_k.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
 
 
 def layers_mode(reps: int = 10):
@@ -1078,6 +1172,8 @@ def main():
         return variants_mode()
     if args.mode == "decode_counters":
         return decode_counters_mode()
+    if args.mode == "decode_split":
+        return decode_split_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
