@@ -100,10 +100,11 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a,
  * apex4_w4a4_gemm_ws without a workspace argument, for callers that cannot
  * allocate device memory: code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc.  Same kernels and the same Y, bit for bit,
- * as apex4_w4a4_gemm_ws; where that call would split K, the partial planes go
- * to a static device array of APEX4_NOALLOC_SCRATCH_BYTES that the library
- * holds on each device it runs on until the process ends.  The call itself
- * allocates nothing (no hipMalloc / hipFree).
+ * as apex4_w4a4_gemm_ws; where that call would split K (the partial planes)
+ * or take the few-row kernel's stream-K form (its counters and parts), the
+ * workspace is a static device array of APEX4_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each device it runs on until the process ends.  The call
+ * itself allocates nothing (no hipMalloc / hipFree).
  *
  *   Arguments and errors as apex4_w4a4_gemm, plus APEX4_ERR_WORKSPACE when the
  *   shape's split would need more than APEX4_NOALLOC_SCRATCH_BYTES (the size
@@ -111,7 +112,9 @@ int apex4_w4a4_gemm(const uint8_t* A_q, const void* s_a,
  *   MI355X every split fits).
  *   All calls on one device share its array: calls that may overlap on one
  *   device (different streams, or host threads) race and must be ordered by
- *   the caller.  Nothing in the array needs clearing between calls.
+ *   the caller.  The caller clears nothing: the stream-K counters are set to
+ *   zero by a fill kernel at the start of every call that uses them, and
+ *   every other byte a call reads it has written first.
  */
 #define APEX4_NOALLOC_SCRATCH_BYTES (32ll << 20)
 int apex4_w4a4_gemm_noalloc(const uint8_t* A_q, const void* s_a,

@@ -212,7 +212,8 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q, int64_t M,
 
 }  // extern "C"
 
-// Split-K partial planes of apex4_w4a4_gemm_noalloc.  Each device holds its own
+// Split-K partial planes (or stream-K counters and parts) of
+// apex4_w4a4_gemm_noalloc.  Each device holds its own
 // copy for the life of the process; host code reaches it only through the
 // address hipGetSymbolAddress returns for the current device (the name itself
 // is a host-side stand-in, not a device address).
@@ -255,8 +256,8 @@ int apex4_w4a4_gemm_noalloc(const uint8_t* A_q, const void* s_a, const uint8_t* 
         rc = scratch_address(&ws);
         if (rc) return rc;
     }
-    // every partial plane element is written before the reduce reads it: the
-    // scratch needs no clearing
+    // every partial plane element is written before the reduce reads it, and
+    // the stream-K counters are cleared by a fill kernel in the launch itself
     return gemm_dispatch(A_q, s_a, W_q, s_w, M, N, K, G, Y, ws, need, apex4::Dump(), false, false, stream);
 }
 
