@@ -190,7 +190,10 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
     constexpr int NT = 64 * NWAVE;
     // groups [glo, ghi) of one or two [32][K/G] blocks (row r at base +
     // min(r, rmax) * K/G) into LDS group-major; a pass covers four 16-byte
-    // vectors per thread (two of each block), all loads issued before the stores
+    // vectors per thread (two of each block), all loads issued before the
+    // stores.  Consecutive lanes take consecutive rows of one vector, so each
+    // 2-byte LDS store of a wave covers 32 consecutive places of a group (row
+    // index fastest there), not 64 places one group-stride apart in one bank.
     auto stage = [&](const uint16_t* b0, int rmax0, uint16_t* d0, const uint16_t* b1, int rmax1, uint16_t* d1, int glo,
                      int ghi) __attribute__((always_inline)) {
         const bool two = b1 != nullptr;
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
                     const int b = two ? (u >> 1) : 0;
                     const int i = i0 + (two ? (u & 1) : u) * NT;
                     if (i < ROWS * nv) {
-                        const int r = i / nv, c = vlo + i - r * nv;
+                        const int r = i & (ROWS - 1), c = vlo + i / ROWS;
                         v[u] = *reinterpret_cast<const uint4*>((b ? b1 : b0) + static_cast<int64_t>(min(r, b ? rmax1 : rmax0)) * ng + 8 * c);
                     }
                 }
@@ -213,7 +216,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
                     const int b = two ? (u >> 1) : 0;
                     const int i = i0 + (two ? (u & 1) : u) * NT;
                     if (i < ROWS * nv) {
-                        const int r = i / nv, c = vlo + i - r * nv;
+                        const int r = i & (ROWS - 1), c = vlo + i / ROWS;
                         const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
                         uint16_t* d = b ? d1 : d0;
 #pragma unroll
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
             const int ngr = ghi - glo;
             for (int b = 0; b < (two ? 2 : 1); ++b)
                 for (int i = tid; i < ngr * ROWS; i += NT) {
-                    const int r = i / ngr, g = glo + i - r * ngr;
+                    const int r = i & (ROWS - 1), g = glo + i / ROWS;
                     (b ? d1 : d0)[g * ROWS + r] = (b ? b1 : b0)[static_cast<int64_t>(min(r, b ? rmax1 : rmax0)) * ng + g];
                 }
         }
@@ -259,7 +262,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         for (int u = 0; u < 2; ++u) {
             const int i = tid + u * 64 * NWAVE;
             if (i < ROWS * nv) {
-                const int r = i / nv, c = i - r * nv;
+                const int r = i & (ROWS - 1), c = i / ROWS;
                 nsc[u] = *reinterpret_cast<const uint4*>(sw + static_cast<int64_t>(min(c0 + r, N - 1)) * ng + 8 * c);
             }
         }
@@ -270,7 +273,7 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         for (int u = 0; u < 2; ++u) {
             const int i = tid + u * 64 * NWAVE;
             if (i < ROWS * nv) {
-                const int r = i / nv, c = i - r * nv;
+                const int r = i & (ROWS - 1), c = i / ROWS;
                 const uint32_t w[4] = {nsc[u].x, nsc[u].y, nsc[u].z, nsc[u].w};
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
