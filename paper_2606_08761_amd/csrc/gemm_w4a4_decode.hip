@@ -385,6 +385,24 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
         const int s_raw = p_lo + wave + NWAVE * pi;
         const bool live = s_raw < p_hi;
         const int s = min(s_raw, p_hi - 1);
+        // The stage's scales are read first, so that their LDS latency overlaps
+        // the fragment reads and the contraction instead of following each
+        // group's MFMAs (a partial last stage's missing groups read a staged
+        // group and are skipped below).
+        float s1v[GPS];
+        uint2 sah[GPS][NR / 4];
+        if (have_sc) {
+#pragma unroll
+            for (int gi = 0; gi < GPS; ++gi) {
+                const int g = GPS == 1 ? (s >> lg) : s * GPS + gi;
+                const int gc = g < ng ? g : ng - 1;
+                const float w1 = h2f(wsc[gc * ROWS + l32]) * (1.0f / 256.0f);
+                s1v[gi] = live ? w1 : 0.f;
+#pragma unroll
+                for (int q4 = 0; q4 < NR / 4; ++q4)
+                    sah[gi][q4] = *reinterpret_cast<const uint2*>(&sas[gc * ROWS + 8 * q4 + 4 * lh]);
+            }
+        }
         i32x4 bw[4], af[4];
         uint4 la[2];
         if constexpr (ALDS) {
@@ -436,14 +454,11 @@ __global__ __launch_bounds__(64 * NWAVE, 1) void w4a4_decode_kernel(
                 }
                 if (!have_sc) continue;
             }
-            const float s1 = live ? h2f(wsc[g * ROWS + l32]) * (1.0f / 256.0f) : 0.f;
+            const float s1 = s1v[gi];
             const float nb = -MAGIC * s1;
-            uint2 sah[4];
-#pragma unroll
-            for (int q4 = 0; q4 < NR / 4; ++q4) sah[q4] = *reinterpret_cast<const uint2*>(&sas[g * ROWS + 8 * q4 + 4 * lh]);
 #pragma unroll
             for (int r = 0; r < NR; ++r) {
-                const uint32_t pair = (r & 2) ? sah[r >> 2].y : sah[r >> 2].x;
+                const uint32_t pair = (r & 2) ? sah[gi][r >> 2].y : sah[gi][r >> 2].x;
                 const uint16_t h = (r & 1) ? static_cast<uint16_t>(pair >> 16) : static_cast<uint16_t>(pair & 0xFFFFu);
                 const float tt = fmaf(__int_as_float(d[r]), s1, nb);
                 acc[r] = fmaf(tt, h2f(h), acc[r]);
