@@ -268,9 +268,10 @@ int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w,
  * the exact int32 sums for G == K), and a second kernel sums the S partials in
  * range order and rounds once to binary16.  With M <= 32 rows, where the
  * 32-column tiles leave more than a tenth of the compute units idle in the last
- * round and the tiles are long (at least 128 stage-groups, i.e. K/128 stages
- * times 128/G groups per stage, below one tile per compute unit; K >= 24576
- * above), the few-row kernel runs in a stream-K form: the full rounds stay
+ * round and the tiles are long (below one tile per compute unit, at least 128
+ * stage-groups, i.e. K/128 stages times 128/G groups per stage, and K >= 24576
+ * once half the compute units or more have a tile; K >= 24576 above), the
+ * few-row kernel runs in a stream-K form: the full rounds stay
  * whole tiles, the remaining tiles' 128-wide K stages are spread evenly over
  * the workgroups, and a tile cut between workgroups has its fp32 parts added in
  * segment order by the workgroup that finishes last (counters cleared by a

@@ -586,9 +586,10 @@ struct DecodeSKPlan {
 };
 // Round robin gives some workgroups one tile more than others.  The stream-K
 // form is taken where it was measured faster: the last round leaves more than a
-// tenth of the CUs idle, and the tiles are long, at least 128 stage-groups
-// (K/128 stages times 128/G groups per stage) below 256 tiles, at least 192
-// stages (K >= 24576) from 256 tiles on.  Below that, a tile's round robin time
+// tenth of the CUs idle, and the tiles are long: below one tile per CU, at
+// least 128 stage-groups (K/128 stages times 128/G groups per stage) and, with
+// half the CUs or more busy, at least 192 stages (K >= 24576); from one tile
+// per CU on, at least 192 stages.  Below that, a tile's round robin time
 // is near the kernel's fixed latency, which the stream-K form's counter clear,
 // count and fix-up only add to.  The first skg workgroups (all, unless there
 // are fewer than 8 units per workgroup) share the units, so each gets at least
@@ -599,7 +600,7 @@ DecodeSKPlan decode_sk_plan(int64_t M, int64_t N, int64_t K, int64_t G) {
     const int64_t rounds = (ntiles + cus - 1) / cus;
     const int64_t gps = G < 128 ? 128 / G : 1;
     if (rounds * cus * 10 <= ntiles * 11) return {0, 0, 0, 0};
-    if (ntiles < cus ? nks * gps < 128 : nks < 192) return {0, 0, 0, 0};
+    if (ntiles < cus ? (nks * gps < 128 || (ntiles * 2 >= cus && nks < 192)) : nks < 192) return {0, 0, 0, 0};
     const int64_t skt = ntiles - ntiles / cus * cus;  // tiles past the full rounds
     const int64_t units = skt * nks;
     const int64_t upw = units / NWAVE;

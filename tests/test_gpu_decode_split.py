@@ -1,7 +1,8 @@
 """The few-row kernel's stream-K form (apex4_w4a4_gemm_ws and the other
 workspace entry points, up to 32 rows).  Where round-robin tiles would leave
-more than a tenth of the CUs idle and the tiles are long (at least 128
-stage-groups below 256 tiles, K >= 24576 from 256 tiles on), the full rounds
+more than a tenth of the CUs idle and the tiles are long (below 256 tiles at
+least 128 stage-groups, and K >= 24576 from 128 tiles on; K >= 24576 from 256
+tiles on), the full rounds
 stay round robin and the remaining tiles' (tile, stage) units are spread evenly
 over the CUs; tiles are cut between workgroups, and the cut tiles' fp32 parts
 are added in segment order through the workspace (Eq. group_decomposition:
@@ -35,7 +36,7 @@ def pk():
 # M = 4, a few tiles over many stages (two tiles: fewer workgroups than CUs),
 # partial last stages (K % 128 != 0), per channel, G = 64 and 256
 SHAPES = [(16, 8448, 24576, 128), (5, 9000, 24576, 128), (17, 8256, 24576, 128), (16, 1024, 8192, 32),
-          (4, 1024, 28672, 32), (2, 300, 8192, 64), (32, 4096, 16384, 256), (3, 100, 16384, 128),
+          (4, 1024, 28672, 32), (2, 300, 8192, 64), (32, 2048, 16384, 256), (3, 100, 16384, 128),
           (7, 1000, 4000, 32), (16, 520, 16480, 16480), (9, 64, 32768, 1024), (16, 64, 8192, 32)]
 
 
@@ -69,10 +70,11 @@ def test_decode_split(O, M, N, K, G):
 
 
 # round robin measured faster: the tile time is near the kernel's fixed latency
-# (K = 8192 at G = 128, whatever the count of tiles; N = 10240 at G = 32), or
-# the last round leaves at most a tenth of the CUs idle (N = 8192, 57344)
+# (K = 8192 at G = 128, whatever the count of tiles; N = 10240 at G = 32; half
+# the CUs busy at K = 8192, G = 32), or the last round leaves at most a tenth
+# of the CUs idle (N = 8192, 57344)
 KEEP = [(16, 10240, 8192, 128), (16, 1024, 8192, 128), (8, 28672, 8192, 128), (16, 10240, 8192, 32),
-        (16, 8192, 28672, 32), (16, 57344, 8192, 128), (2, 300, 2048, 64)]
+        (16, 8192, 28672, 32), (16, 57344, 8192, 128), (2, 300, 2048, 64), (16, 4096, 8192, 32)]
 
 
 @pytest.mark.parametrize("M,N,K,G", KEEP)
