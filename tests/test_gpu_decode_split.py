@@ -34,10 +34,12 @@ def pk():
 # over many workgroups, and tens of them), the mixed configuration's G = 32
 # value projection (N = 1024) at M = 16 and its down projection (K = 28672) at
 # M = 4, a few tiles over many stages (two tiles: fewer workgroups than CUs),
-# partial last stages (K % 128 != 0), per channel, G = 64 and 256
+# partial last stages (K % 128 != 0, also past full rounds), per channel,
+# G = 64, 256 and 512, and the 8-row form at its largest M
 SHAPES = [(16, 8448, 24576, 128), (5, 9000, 24576, 128), (17, 8256, 24576, 128), (16, 1024, 8192, 32),
           (4, 1024, 28672, 32), (2, 300, 8192, 64), (32, 2048, 16384, 256), (3, 100, 16384, 128),
-          (7, 1000, 4000, 32), (16, 520, 16480, 16480), (9, 64, 32768, 1024), (16, 64, 8192, 32)]
+          (7, 1000, 4000, 32), (16, 520, 16480, 16480), (9, 64, 32768, 1024), (16, 64, 8192, 32),
+          (8, 2048, 16384, 512), (3, 8448, 24608, 32)]
 
 
 @pytest.mark.parametrize("M,N,K,G", SHAPES)
