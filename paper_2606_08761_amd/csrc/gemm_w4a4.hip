@@ -494,24 +494,55 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
         };
         read_f(0, af[0]);
         uint2 swh[NJ][4];
-        static_for<0, NF>([&](auto F) __attribute__((always_inline)) {
-            constexpr int f = decltype(F)::value;
-            constexpr int gi = f / MI, i = f % MI;
-            if constexpr (f + 1 < NF) read_f(f + 1, af[(f + 1) & 1]);
-            if constexpr (i == 0) {
+        // At G = 32 an item (block f, column block j) is a single MFMA, so item
+        // t + 1's MFMA is issued before item t is dequantized, into the other
+        // of two result sets: the dequantization then overlaps the next MFMA
+        // instead of waiting for its own (with one result set every MFMA also
+        // waited for the previous dequantization to read its registers).  At
+        // G = 64 (two chained MFMAs per item) a second set brought nothing, and
+        // in the debug and partial-last-stage forms it only adds spills.
+        if constexpr (GPS == 4 && !DUMP && !TAIL) {
+            constexpr int NIT = NF * NJ;
+            i32x16 dd[2];
+            auto issue = [&](auto T) __attribute__((always_inline)) {
+                constexpr int t = decltype(T)::value;
+                constexpr int f = t / NJ, j = t % NJ, gi = f / MI;
+                dd[t & 1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][gi], af[f & 1][0], start, 0, 0, 0);
+            };
+            issue(std::integral_constant<int, 0>());
+            static_for<0, NIT>([&](auto T) __attribute__((always_inline)) {
+                constexpr int t = decltype(T)::value;
+                constexpr int f = t / NJ, j = t % NJ, gi = f / MI, i = f % MI;
+                if constexpr (j == 0) {
+                    if constexpr (f + 1 < NF) read_f(f + 1, af[(f + 1) & 1]);
+                    if constexpr (i == 0) {
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) read_sw(buf, j, swh[j], gi);
-            }
+                        for (int jj = 0; jj < NJ; ++jj) read_sw(buf, jj, swh[jj], gi);
+                    }
+                }
+                if constexpr (t + 1 < NIT) issue(std::integral_constant<int, t + 1>());
+                dequant(dd[t & 1], acc[i][j], read_sa(buf, i, gi), swh[j]);
+            });
+        } else {
+            static_for<0, NF>([&](auto F) __attribute__((always_inline)) {
+                constexpr int f = decltype(F)::value;
+                constexpr int gi = f / MI, i = f % MI;
+                if constexpr (f + 1 < NF) read_f(f + 1, af[(f + 1) & 1]);
+                if constexpr (i == 0) {
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                i32x16 d = start;
+                    for (int j = 0; j < NJ; ++j) read_sw(buf, j, swh[j], gi);
+                }
 #pragma unroll
-                for (int q = 0; q < KPG; ++q)
-                    d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][gi * KPG + q], af[f & 1][q], d, 0, 0, 0);
-                dump_block(d, i, j, ks * GPS + gi);
-                dequant(d, acc[i][j], read_sa(buf, i, gi), swh[j]);
-            }
-        });
+                for (int j = 0; j < NJ; ++j) {
+                    i32x16 d = start;
+#pragma unroll
+                    for (int q = 0; q < KPG; ++q)
+                        d = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[j][gi * KPG + q], af[f & 1][q], d, 0, 0, 0);
+                    dump_block(d, i, j, ks * GPS + gi);
+                    dequant(d, acc[i][j], read_sa(buf, i, gi), swh[j]);
+                }
+            });
+        }
     };
 
     // End of a group for the persistent mode.
