@@ -48,7 +48,7 @@ def parse():
     p.add_argument("--no-decode", action="store_true", help="skip the decode-size linears")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample duration")
     p.add_argument("--mode", choices=("bench", "counters", "rho", "summarize", "gsweep", "power", "layers", "variants",
-                                      "decode_counters", "decode_split"),
+                                      "decode_counters", "decode_split", "decode_sq"),
                    default="bench",
                    help="counters: 3 GEMM launches + 3 copies of 256 MiB, for rocprofv3 --pmc; "
                         "rho: the intra-CU throughput probes; "
@@ -74,6 +74,9 @@ def parse():
     p.add_argument("--decode-trace-csv", help="summarize: kernel_trace.csv of the --kernel-trace run of --mode decode_counters")
     p.add_argument("--decode-log", help="summarize: output of --mode decode_counters (its JSON line)")
     p.add_argument("--decode-commands", help="summarize: text file with the commands that made the --decode-* files")
+    p.add_argument("--decode-sq-csv", nargs="*",
+                   help="summarize: counter_collection.csv files of SQ passes over --mode decode_sq")
+    p.add_argument("--decode-sq-commands", help="summarize: text file with the commands that made --decode-sq-csv")
     p.add_argument("--layers-command", default="python3 bench.py --mode layers", help="summarize: the command that made --layers-log")
     return p.parse_args()
 
@@ -177,6 +180,9 @@ def summarize_mode(args):
             summarize_power(args.power_log, args.power_command)
         if args.rho_json:
             summarize_rho(args.rho_json, args.rho_command)
+        if args.decode_sq_csv:
+            summarize_decode_sq(args.decode_sq_csv,
+                                open(args.decode_sq_commands).read().strip() if args.decode_sq_commands else "")
         return
     copy_kib = (256 << 20) / 1024.0
     fetch = per_kernel(args.fetch_csv, "FETCH_SIZE")
@@ -639,6 +645,56 @@ def summarize_sq_variants(paths, cmds):
         if "GRBM_GUI_ACTIVE" in c and "SQ_INSTS_MFMA" in c:
             lines += [f"## {title}", ""] + _sq_section(c, title.split(" (")[0], mfma) + [""]
     with open(os.path.join(ROOT, "profiles", "gemm_variants_sq_paper_shape.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+# (label, M, N, K, G, tiled, kernel instantiation the plan picks: MROWS, ring depth, groups per stage)
+DECODE_SQ = [("G=32, K=28672: the mixed configuration's down projection", 16, 8192, 28672, 32, False, "<16, 4, 4,"),
+             ("G=128, N=K=8192, tiled weights", 16, 8192, 8192, 128, True, "<16, 6, 1,"),
+             ("G=128, N=28672, K=8192, tiled weights, activations staged in LDS", 32, 28672, 8192, 128, True,
+              "<32, 6, 1,")]
+
+
+def decode_sq_mode(reps: int = 5):
+    """Each DECODE_SQ few-row GEMM `reps` times (random codes and scales), for
+    SQ counter passes; every case runs its own instantiation of the few-row
+    kernel, which the summary tells apart by name."""
+    import torch
+    import paper_2606_08761_amd as pk
+    from paper_2606_08761_amd import workloads as wl
+    dev = torch.device("cuda", 0)
+    for (label, Md, Nd, Kd, Gd, tiled, _) in DECODE_SQ:
+        r = wl.rng_for("decode", 11, Md * 7 + Nd + Kd + Gd)
+        Wq = torch.from_numpy(wl.random_codes(r, Nd, Kd)).to(dev)
+        W = pk.apex4_tile_weights(Wq) if tiled else Wq
+        sw = torch.from_numpy(wl.random_scales(r, Nd, Kd // Gd)).to(dev)
+        Aq = torch.from_numpy(wl.random_codes(r, Md, Kd)).to(dev)
+        sa = torch.from_numpy(wl.random_scales(r, Md, Kd // Gd)).to(dev)
+        Y = torch.empty((Md, Nd), dtype=torch.float16, device=dev)
+        for _ in range(reps):
+            if tiled:
+                pk.apex4_w4a4_gemm_tiled(Aq, sa, W, sw, Gd, None, Y)
+            else:
+                pk.apex4_w4a4_gemm(Aq, sa, W, sw, Gd, Y)
+        torch.cuda.synchronize()
+        plan = pk.apex4_w4a4_gemm_plan("gemm", Md, Nd, Kd, Gd, pk.APEX4_DEBUG_W_TILED if tiled else 0)
+        print(json.dumps({"mode": "decode_sq", "case": label, "M": Md, "N": Nd, "K": Kd, "G": Gd, "plan": plan}),
+              flush=True)
+
+
+def summarize_decode_sq(paths, cmds):
+    """profiles/decode_sq.md: where the SIMD cycles of the few-row kernel go
+    (bench.py --mode decode_sq)."""
+    lines = ["# Few-row GEMM (M = 16 and 32): SQ counters", "",
+             "Commands (run from the repository root on one MI355X):", "", "```", cmds, "```", "",
+             "Means over the launches of each case. The kernel fills the CUs with one 8-wave workgroup each; "
+             "shares are of the kernel's cycles per SIMD.", ""]
+    for (label, Md, Nd, Kd, Gd, tiled, key) in DECODE_SQ:
+        c = _sq_means(paths, lambda n, key=key: "w4a4_decode_kernel" in n and key in n)
+        if "GRBM_GUI_ACTIVE" in c and "SQ_INSTS_MFMA" in c:
+            lines += [f"## M={Md} N={Nd} K={Kd} {label}", ""]
+            lines += _sq_section(c, f"w4a4_decode_kernel{key.rstrip(',')}...>", "v_mfma_i32_32x32x32_i8") + [""]
+    with open(os.path.join(ROOT, "profiles", "decode_sq.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
 
@@ -1174,6 +1230,8 @@ def main():
         return decode_counters_mode()
     if args.mode == "decode_split":
         return decode_split_mode()
+    if args.mode == "decode_sq":
+        return decode_sq_mode()
     if args.mode == "rho":
         from paper_2606_08761_amd import rho
         print(json.dumps(rho.measure()), flush=True)
