@@ -22,7 +22,8 @@
 //     exact group sum.  Every partial satisfies |256 P| <= 2^21, so the
 //     1.5 * 2^23 accumulator bias gives the float conversion for free at every G.
 //     The weight scale is one value per lane.  The activation scales of all rows
-//     and groups (at most 32 * K/G binary16) sit in LDS for the whole kernel.
+//     and groups (at most 32 * K/G binary16) sit in LDS for the whole kernel
+//     (for the stream-K form with fewer tiles than workgroups, per segment).
 //   * Groups of 32 or 64 (GPS = 4 or 2 groups per 128-wide stage): each MFMA
 //     must stay inside one group, so lane half h of MFMA kk covers
 //     k in [32 kk + 16 h, 32 kk + 16 h + 16) (packed bytes 16 kk + 8 h .. + 7)
@@ -49,6 +50,17 @@
 //   * The 8 partial fp32 tiles are reduced through LDS in passes of 8 output
 //     registers per lane (two passes at M > 16), which keeps the reduction
 //     buffer at 16 KB.
+//   * Scales are staged into LDS with consecutive lanes on consecutive rows of
+//     one 16-byte vector, so a wave's 2-byte stores land in consecutive places
+//     of a group (one group stride apart they would all hit one bank), and a
+//     stage reads all its groups' scales before its MFMAs.
+//   * Stream-K (workspace entry points): where the round-robin walk leaves
+//     CUs idle in its last round and the tiles are long, the workgroups keep
+//     the full rounds and split the remaining tiles' (tile, stage) units into
+//     equal runs; a tile cut between workgroups has its fp32 parts added in
+//     segment order, through the workspace, by the workgroup that counts its
+//     last part.  With fewer tiles than workgroups the scales are staged per
+//     segment, only for the groups it covers.
 //   * DUMP: each stage's exact partial group sums of rows [pm0, pm0 + pmr) are
 //     added with integer atomics into the zeroed P[pmr][N][K/G] (the sum over a
 //     group's stages is exact in any order); sa == nullptr skips the scales
