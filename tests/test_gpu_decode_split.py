@@ -14,7 +14,10 @@ sums).
     from a replayed graph (the counters are cleared by a kernel each call);
   * the exact group sums (debug dump with the workspace) against the oracle;
   * tiled and row-major weights give the same bits (same kernel, same cuts);
-  * shapes where the round-robin form was measured faster keep it.
+  * shapes where the round-robin form was measured faster keep it;
+  * 200 back-to-back calls on one workspace, alternating two input sets, each
+    give their own set's bits (the parts and counters cross XCDs through
+    device-scope accesses, without a full fence).
 """
 import numpy as np
 import pytest
@@ -115,3 +118,38 @@ def test_decode_split_graph_replay():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(Y, ref), i
+
+
+@pytest.mark.parametrize("M,N,K,G", [(16, 1024, 8192, 32), (5, 9000, 24576, 128), (16, 64, 8192, 32)])
+def test_decode_split_many_calls(M, N, K, G):
+    """Many back-to-back calls on one workspace, alternating between two input
+    sets, each give the bits of their own input set.
+
+    Each call's cut tiles are added up by whichever workgroup counts their last
+    part, reading parts that other workgroups (on any XCD) wrote with
+    device-scope stores.  A part read before it was written would hold the
+    previous call's part, which comes from the other input set, and a stale
+    counter would leave a tile unwritten or written twice; either would change
+    some output of some call."""
+    import torch
+    m = pk()
+    assert m.apex4_w4a4_gemm_plan("gemm_ws", M, N, K, G) == ("decode_split", 1)
+    sets = []
+    for seed in (1, 2):
+        r = np.random.default_rng(M * 31 + N + K + G + seed)
+        Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+        sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+        sets.append([dev(a) for a in (Aq, sa, Wq, sw)])
+    ws = torch.empty((m.apex4_w4a4_gemm_workspace_size(M, N, K, G),), dtype=torch.uint8, device="cuda")
+    refs = [m.apex4_w4a4_gemm(*d, G) for d in sets]   # round robin, no workspace
+    refs_ws = [m.apex4_w4a4_gemm_ws(*d, G, ws) for d in sets]
+    torch.cuda.synchronize()
+    assert not torch.equal(refs_ws[0], refs_ws[1])
+    for a, b in zip(refs, refs_ws):
+        check_tolerance(host(b), host(a).astype(np.float64), f"stream-K vs round robin {M}x{N}x{K}")
+    outs = [torch.empty_like(refs_ws[0]) for _ in range(200)]
+    for i, Y in enumerate(outs):
+        m.apex4_w4a4_gemm_ws(*sets[i & 1], G, ws, Y)
+    torch.cuda.synchronize()
+    bad = [i for i, Y in enumerate(outs) if not torch.equal(Y, refs_ws[i & 1])]
+    assert not bad, f"{len(bad)} of {len(outs)} calls differ, first {bad[:5]}"
