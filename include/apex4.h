@@ -167,7 +167,7 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
 #define APEX4_ENTRY_GEMM 0    /* apex4_w4a4_gemm (and _debug without workspace) */
 #define APEX4_ENTRY_GEMM_WS 1 /* apex4_w4a4_gemm_ws (and _debug with workspace) */
 #define APEX4_ENTRY_LINEAR 2  /* apex4_w4a4_linear (and _debug); its GEMM, after the quantizer */
-#define APEX4_KERNEL_GEMV 1       /* one row: v_dot8 on the packed codes */
+#define APEX4_KERNEL_GEMV 1       /* one row (two on tiled weights): v_dot8 on the packed codes */
 #define APEX4_KERNEL_FUSED 2      /* one row: quantizer fused into the GEMV's prologue */
 #define APEX4_KERNEL_DECODE 3     /* up to 32 rows: weights streamed once through the MFMA */
 #define APEX4_KERNEL_TILE_64 4    /* 64 x 128 output tiles */
