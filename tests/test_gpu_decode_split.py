@@ -17,7 +17,9 @@ sums).
   * shapes where the round-robin form was measured faster keep it;
   * 200 back-to-back calls on one workspace, alternating two input sets, each
     give their own set's bits (the parts and counters cross XCDs through
-    device-scope accesses, without a full fence).
+    device-scope accesses, without a full fence);
+  * seeded random few-row shapes, whichever form the plan picks, against the
+    oracle in full.
 """
 import numpy as np
 import pytest
@@ -153,3 +155,51 @@ def test_decode_split_many_calls(M, N, K, G):
     torch.cuda.synchronize()
     bad = [i for i, Y in enumerate(outs) if not torch.equal(Y, refs_ws[i & 1])]
     assert not bad, f"{len(bad)} of {len(outs)} calls differ, first {bad[:5]}"
+
+
+def _random_shapes(n=14, seed=2024):
+    """Seeded (M, N, K, G) draws over the few-row range, K a multiple of G
+    (not always of 128), sized so the oracle covers every output in seconds."""
+    r = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        G = int(r.choice([32, 64, 128, 256, 0]))
+        K = int(r.integers(32, 257)) * 64
+        if G == 0:
+            G = K
+        K -= K % G
+        if K < G:
+            continue
+        M, N = int(r.integers(2, 33)), int(r.integers(1, 129)) * 32 - int(r.integers(0, 32))
+        if M * N * K > 1.2e9:
+            continue
+        out.append((M, N, K, G))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K,G", _random_shapes())
+def test_decode_workspace_random_shapes(O, M, N, K, G):
+    """Random few-row shapes through the workspace entry point, whichever form
+    the plan picks: every output within the tolerance of the oracle, the exact
+    group sums of a row window, the same bits on a second call, and a
+    workspace of at most 3 MB."""
+    import torch
+    m = pk()
+    kern, S = m.apex4_w4a4_gemm_plan("gemm_ws", M, N, K, G)
+    need = m.apex4_w4a4_gemm_workspace_size(M, N, K, G)
+    log(f"random decode M={M} N={N} K={K} G={G}: {(kern, S)}, workspace {need} bytes")
+    assert kern in ("decode", "decode_split") and S == 1
+    assert (need > 0) == (kern == "decode_split") and need <= 3 << 20
+    r = np.random.default_rng(M * 131 + N * 7 + K + G)
+    Aq, Wq = wl.random_codes(r, M, K), wl.random_codes(r, N, K)
+    sa, sw = wl.random_scales(r, M, K // G), wl.random_scales(r, N, K // G)
+    d = [dev(a) for a in (Aq, sa, Wq, sw)]
+    ws = torch.empty((max(need, 16),), dtype=torch.uint8, device="cuda")
+    Y = m.apex4_w4a4_gemm_ws(*d, G, ws)
+    Y2 = m.apex4_w4a4_gemm_ws(*d, G, ws)
+    m0, mr = M // 3, min(4, M - M // 3)
+    Yd, P = m.apex4_w4a4_gemm_debug(*d, G, m0, mr, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Y2, Y) and torch.equal(Yd, Y)
+    assert np.array_equal(host(P), O.groupsums(Aq, Wq, K, G, m0, mr))
+    check_tolerance(host(Y), O.gemm_rows(Aq, sa, Wq, sw, K, G), f"random decode {M}x{N}x{K} G{G}")
