@@ -137,7 +137,7 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
                               int64_t m0, int64_t mr, int32_t* P, void* stream);
 
 /* flags of apex4_w4a4_gemm_debug (and of apex4_w4a4_gemm_plan, apex4_w4a4_linear_debug) */
-#define APEX4_DEBUG_GENERAL_TILES 1 /* tile kernel only: no one-row, few-row or G = 128 ping-pong kernel */
+#define APEX4_DEBUG_GENERAL_TILES 1 /* tile kernel only: no one-row, few-row or ping-pong (G = 128, 256) kernel */
 #define APEX4_DEBUG_W_TILED 2       /* W_q is in the tiled layout of apex4_tile_weights */
 
 /*
@@ -172,7 +172,7 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
 #define APEX4_KERNEL_DECODE 3     /* up to 32 rows: weights streamed once through the MFMA */
 #define APEX4_KERNEL_TILE_64 4    /* 64 x 128 output tiles */
 #define APEX4_KERNEL_TILE_128 5   /* 128 x 256 output tiles */
-#define APEX4_KERNEL_PINGPONG 6   /* G = 128 on 128 x 256 tiles, MFMA and dequant waves alternating */
+#define APEX4_KERNEL_PINGPONG 6   /* G = 128 or 256 on 128 x 256 tiles, MFMA and dequant waves alternating */
 #define APEX4_KERNEL_DECODE_SPLIT 7 /* up to 32 rows, stream-K over the CUs (workspace entry points) */
 
 /*

@@ -47,9 +47,9 @@
 //   * Workgroup ids are remapped so that each XCD (8 per MI355X, each with its
 //     own L2) works on a compact block of output tiles (8 m-tiles by a band of
 //     n-tiles at a time).
-//   * G == 128 on 128 x 256 tiles runs w4a4_gemm_pp_kernel: the same wave tile
-//     and arithmetic, with the two waves of each SIMD running their MFMA and
-//     dequant phases half a stage apart (described at the kernel).  Small tiles
+//   * G in {128, 256} on 128 x 256 tiles runs w4a4_gemm_pp_kernel: the same
+//     wave tile and arithmetic, with the two waves of each SIMD running their
+//     MFMA and dequant phases half a stage apart (described at the kernel).  Small tiles
 //     (64 x 128) may split K over two wave groups (KSPLIT) and keep PF stages
 //     of loads in flight.
 //   * Split-K across workgroups (launch_gemm_splitk, caller workspace): when
@@ -719,7 +719,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
     }
 }
 
-// G = 128 on 128 x 256 tiles with a ping-pong schedule.
+// G = 128 (and 256) on 128 x 256 tiles with a ping-pong schedule.
 //
 // Each SIMD runs one wave of group X (waves 0-3) and one of group Y (waves
 // 4-7), which own the same 128 x 32 outputs per wave as the kernel above.  A
@@ -746,9 +746,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KSPLIT, 1) void w4a4_gemm_
 //     free: weights of stage s + 1 right after stage s's are widened, its A
 //     chunk of stage s + 2 right after stage s + 1's is stored (two slots of
 //     cover each).
-//   * DUMP: the group sums of rows [pm0, pm0 + pmr) also go to P[pmr][N][K/128]
+//   * SPG: stages per group (1 for G = 128, 2 for G = 256).  The group's
+//     stages accumulate into the same sums from the bias (|256 P| <= 2^22 at
+//     G = 256, so the bias still converts exactly); only its last stage reads
+//     the scales and has a dequant phase, which is skipped in the others, as
+//     the kernel above does in its persistent mode.
+//   * DUMP: the group sums of rows [pm0, pm0 + pmr) also go to P[pmr][N][K/G]
 //     in the dequant phase (sa == nullptr: no scales read, no Y written).
-template <bool DUMP>
+template <bool DUMP, int SPG>
 __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const uint8_t* __restrict__ Aq, const uint16_t* __restrict__ sa, const uint8_t* __restrict__ Wq,
     const uint16_t* __restrict__ sw, int M, int N, int K, uint16_t* __restrict__ Y, int nks_split,
@@ -783,7 +788,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     // K range: stages [kofs, kofs + nks) of this workgroup's split (blockIdx.y)
     const int nks = nks_split;
     const int kofs = static_cast<int>(blockIdx.y) * nks_split;
-    const int ng = K / 128;
+    const int ng = K / (KS * SPG);
 
     // this thread's 16-byte chunk of A per stage and its widened LDS places
     const int ar = tid >> 2, ap = tid & 3;
@@ -807,7 +812,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     auto load_a = [&](int ks) __attribute__((always_inline)) {
         ks = min(ks, nks - 1) + kofs;
         ra = *reinterpret_cast<const uint4*>(Aq + static_cast<int64_t>(ks) * (KS / 2) + a_off);
-        rsc = have_sc ? sc_base[sc_off + static_cast<uint32_t>(ks)] : static_cast<uint16_t>(0);
+        rsc = have_sc ? sc_base[sc_off + static_cast<uint32_t>(ks / SPG)] : static_cast<uint16_t>(0);
     };
     auto store_a = [&](int buf) __attribute__((always_inline)) {
         *reinterpret_cast<i32x4*>(&st[buf].a[a_lds0]) = frag2(ra.x, ra.y);
@@ -832,12 +837,15 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     const i32x16 start = splat16(static_cast<int>(MAGIC_BITS));
 
     // MFMA phase of stage s (LDS buffer and register slot s & 1)
-    auto mfma_phase = [&](int s, int par) __attribute__((always_inline)) {
+    auto mfma_phase = [&](int s, int par, auto FIRST, auto LAST) __attribute__((always_inline)) {
+        constexpr bool first = decltype(FIRST)::value, last = decltype(LAST)::value;
         const int c = BM + wave * 32 + 4 * lh;
+        if constexpr (last) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[par].scale[0][c + 8 * q]);
+            for (int q = 0; q < 4; ++q) swh[q] = *reinterpret_cast<const uint2*>(&st[par].scale[0][c + 8 * q]);
 #pragma unroll
-        for (int i = 0; i < MI; ++i) sav[i] = h2f(st[par].scale[0][i * 32 + l32]) * (1.0f / 256.0f);
+            for (int i = 0; i < MI; ++i) sav[i] = h2f(st[par].scale[0][i * 32 + l32]) * (1.0f / 256.0f);
+        }
         i32x4 bw[KK];
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
@@ -861,7 +869,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
             constexpr int n = decltype(NN)::value;
             if constexpr (n + LA < 4 * MI) af[(n + LA) % (LA + 1)] = frag(n + LA);
             constexpr int kk = n >> 2, i = n & 3;
-            D[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[kk], af[n % (LA + 1)], kk == 0 ? start : D[i], 0, 0, 0);
+            D[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bw[kk], af[n % (LA + 1)], (kk == 0 && first) ? start : D[i], 0, 0, 0);
         });
         // keep that order: LA fragment reads, then MFMA / next read pairs
         __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
@@ -876,7 +884,7 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
 #pragma unroll
         for (int i = 0; i < MI; ++i) asm volatile("" : "+v"(D[i]));
         if constexpr (DUMP) {
-            const int g = kofs + s;
+            const int g = (kofs + s) / SPG;
 #pragma unroll
             for (int i = 0; i < MI; ++i) {
                 const int gm = m0 + i * 32 + l32;
@@ -931,12 +939,19 @@ __global__ __launch_bounds__(512, 1) void w4a4_gemm_pp_kernel(
     // barrier that ends its phase (or hoisted above the one that starts it).
     auto pin = [](auto& v) __attribute__((always_inline)) { asm volatile("" : "+v"(v)); };
     for (int s = 0; s < nks; ++s) {
-        mfma_phase(s, s & 1);
+        // a group's stages accumulate into D from the bias; the group's last
+        // stage reads its scales and is dequantized
+        if constexpr (SPG == 1) {
+            mfma_phase(s, s & 1, std::true_type(), std::true_type());
+        } else {
+            if (s % SPG == 0) mfma_phase(s, s & 1, std::true_type(), std::false_type());
+            else mfma_phase(s, s & 1, std::false_type(), std::true_type());
+        }
 #pragma unroll
         for (int i = 0; i < MI; ++i) pin(D[i]);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
-        dequant_phase(s);
+        if (SPG == 1 || s % SPG == SPG - 1) dequant_phase(s);
 #pragma unroll
         for (int i = 0; i < MI; ++i) pin(acc[i]);
         stage_next(s + ahead);
@@ -1064,8 +1079,9 @@ hipError_t launch(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, cons
                                                                              stream, S, part);
 }
 
-// The G = 128 ping-pong kernel on 128 x 256 tiles (S > 1: split over K, fp32
-// partial tiles to part).
+// The ping-pong kernel on 128 x 256 tiles, SPG stages per group (S > 1, for
+// G = 128 only: split over K, fp32 partial tiles to part).
+template <int SPG>
 hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                      int64_t N, int64_t K, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
                      float* part = nullptr) {
@@ -1074,10 +1090,10 @@ hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, c
     const dim3 grid(static_cast<unsigned>(tiles), static_cast<unsigned>(S));
     const int m = static_cast<int>(M), n = static_cast<int>(N), k = static_cast<int>(K), nks = static_cast<int>(K / KS / S);
     if (dump.P)
-        hipLaunchKernelGGL(w4a4_gemm_pp_kernel<true>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
+        hipLaunchKernelGGL((w4a4_gemm_pp_kernel<true, SPG>), grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
                            dump.P, dump.m0, dump.mr, wt ? 1 : 0);
     else
-        hipLaunchKernelGGL(w4a4_gemm_pp_kernel<false>, grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
+        hipLaunchKernelGGL((w4a4_gemm_pp_kernel<false, SPG>), grid, dim3(512), 0, stream, Aq, sa, Wq, sw, m, n, k, Y, nks, part,
                            static_cast<int32_t*>(nullptr), 0, 0, wt ? 1 : 0);
     return hipGetLastError();
 }
@@ -1087,8 +1103,8 @@ hipError_t launch_pp(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, c
 // Tile: 128 x 256 per workgroup, 8 waves (two per SIMD) of 128 x 32.  When that
 // tiling would not give every CU a workgroup, 64 x 128 tiles with 4 waves of
 // 64 x 32 (four times as many workgroups, two per CU), or 8 waves splitting K
-// (see launch).  G = 128 on 128 x 256 tiles is the ping-pong kernel unless
-// force_general.
+// (see launch).  G = 128 (and G = 256 unsplit) on 128 x 256 tiles is the
+// ping-pong kernel unless force_general.
 template <int WAVES_N, int MI>
 hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq, const uint16_t* sw, int64_t M,
                         int64_t N, int64_t K, int64_t G, uint16_t* Y, Dump dump, bool wt, hipStream_t stream, int S = 1,
@@ -1099,11 +1115,17 @@ hipError_t launch_tiles(const uint8_t* Aq, const uint16_t* sa, const uint8_t* Wq
     if (G == 128) {
         if constexpr (WAVES_N == 8 && MI == 4) {
             if (!force_general)
-                return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, S, static_cast<float*>(part));
+                return launch_pp<1>(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, S, static_cast<float*>(part));
         }
         return launch<1, WAVES_N, MI, 1, kRotate, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
     }
-    if (G == 256) return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
+    if (G == 256) {
+        if constexpr (WAVES_N == 8 && MI == 4) {
+            if (!force_general && S == 1)
+                return launch_pp<2>(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, 1, nullptr);
+        }
+        return launch<1, WAVES_N, MI, 1, kPersist, true>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
+    }
     return launch<1, WAVES_N, MI, 1, kPersist, false>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, S, part);
 }
 
@@ -1235,7 +1257,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int64_t G, bool split, bool 
         return {split && decode_split_workspace_bytes(M, N, K, G) > 0 ? kKernelDecodeSplit : kKernelDecode, 1};
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 255) / 256);
     if (big_tiles < device_cu_count()) return {kKernelTile64, 1};
-    return {G == 128 && !force_tile ? kKernelPingPong : kKernelTile128, 1};
+    return {(G == 128 || G == 256) && !force_tile ? kKernelPingPong : kKernelTile128, 1};
 }
 
 namespace {
@@ -1251,7 +1273,9 @@ hipError_t launch_planned(const GemmPlan& plan, const uint8_t* Aq, const uint16_
             return launch_tiles<4, 2>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, plan.splits, part);
         case kKernelTile128:
             return launch_tiles<8, 4>(Aq, sa, Wq, sw, M, N, K, G, Y, dump, wt, stream, 1, nullptr, /*force_general=*/true);
-        case kKernelPingPong: return launch_pp(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, plan.splits, part);
+        case kKernelPingPong:
+            return G == 256 ? launch_pp<2>(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, plan.splits, part)
+                            : launch_pp<1>(Aq, sa, Wq, sw, M, N, K, Y, dump, wt, stream, plan.splits, part);
         default: return hipErrorInvalidValue;
     }
 }

@@ -100,7 +100,8 @@ def test_paper_shape_groupsums_pingpong(O, paper, m0):
 
 def test_pingpong_equals_general_tiles(O, paper):
     """The ping-pong schedule changes when work is issued, not the arithmetic:
-    the same Y and P bits as the general 128 x 256 tile kernel."""
+    the same Y and P bits as the general 128 x 256 tile kernel (also at G = 256,
+    where its group spans two stages, on the shapes below)."""
     import torch
     m = pk()
     G = paper["G"]
@@ -111,8 +112,10 @@ def test_pingpong_equals_general_tiles(O, paper):
     assert torch.equal(Pg, Pp)
 
 
-# ragged shapes on 128 x 256 tiles, and split-K shapes (G = 128)
-PP_SHAPES = [(1111, 8200, 640, 128), (1500, 8195, 1152, 128), (2050, 4100, 4096, 128), (4096, 4096, 1024, 128)]
+# ragged shapes on 128 x 256 tiles (G = 128, and G = 256: two stages per
+# group), and split-K shapes (G = 128)
+PP_SHAPES = [(1111, 8200, 640, 128), (1500, 8195, 1152, 128), (2050, 4100, 4096, 128), (4096, 4096, 1024, 128),
+             (1111, 8200, 1280, 256), (2050, 4100, 4096, 256), (4096, 4096, 512, 256)]
 PP_SPLIT = [(256, 8192, 8192, 128), (512, 4096, 8192, 128), (300, 2000, 4096, 128)]
 
 
@@ -245,7 +248,7 @@ def test_granularity_sweep_groupsums(O, G):
     x = wl.activations(wl.rng_for("gsweep", 1, G), M, K)
     A = Quantized(O, x, G)
     kern = m.apex4_w4a4_gemm_plan("gemm", M, N, K, G)
-    assert kern == (("pingpong" if G == 128 else "tile128"), 1)
+    assert kern == (("pingpong" if G in (128, 256) else "tile128"), 1)
     Y = m.apex4_w4a4_gemm(A.q_d, A.s_d, W.q_d, W.s_d, G)
     for m0, mr in windows(M):
         Yd, P = m.apex4_w4a4_gemm_debug(A.q_d, A.s_d, W.q_d, W.s_d, G, m0, mr)
