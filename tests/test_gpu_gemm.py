@@ -395,6 +395,44 @@ def test_w4a4_linear_module_streams(O):
         check_tolerance(host(yy), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), "module two streams")
 
 
+def test_w4a4_linear_module_graph(O):
+    """The drop-in layer captured in a graph, as a serving loop would: one row
+    (the fused kernel), 16 rows (the few-row kernel's stream-K form) and 64
+    rows (split over K), each with the layer's own work buffers.  Three
+    replays with eager calls of the same layer in between each give the eager
+    bits, and those are within the oracle's tolerance."""
+    import torch
+    m = pk()
+    N, K, G = 1024, 8192, 32
+    x, w = wl.float_workload("tiny", 64, N, K)
+    lin = m.W4A4Linear(dev(w), G)
+    xs = {r: dev(x[:r]) for r in (1, 16, 64)}
+    plans = {r: m.apex4_w4a4_gemm_plan("gemm_ws", r, N, K, G) for r in (16, 64)}
+    log(f"module graph: plans {plans}")
+    assert plans[16] == ("decode_split", 1) and plans[64][1] > 1
+    eager = {r: lin(xs[r]) for r in xs}
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        outs = {r: lin(xs[r]) for r in xs}
+    torch.cuda.synchronize()
+    for i in range(3):
+        for yy in outs.values():
+            yy.fill_(float("nan"))
+        again = {r: lin(xs[r]) for r in xs}   # eager work on the device between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for r in xs:
+            assert torch.equal(outs[r], eager[r]) and torch.equal(again[r], eager[r]), (i, r)
+    Wq_o, sw_o = O.quantize(w, G)
+    for r in xs:
+        Aq_o, sa_o = O.quantize(x[:r], G)
+        check_tolerance(host(eager[r]), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"module graph rows={r}")
+
+
 def test_weights_just_under_4gib(O):
     """The largest weight operand the ABI accepts: N K/2 = 4,294,950,912 bytes,
     16 KiB under 2^32 (the kernels address operand rows with 32-bit byte
