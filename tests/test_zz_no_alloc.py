@@ -3,7 +3,9 @@ per-device scratch in place of a caller workspace (for callers that cannot
 allocate).  Its Y must equal apex4_w4a4_gemm_ws's bit for bit (same kernels,
 same split or stream-K cuts), and the oracle's within tolerance, on
 consecutive calls that share the scratch, the second with a smaller problem (a
-stale partial or counter from the first call would show up in it).
+stale partial or counter from the first call would show up in it), and
+captured in a graph whose replays, with eager calls between, give the eager
+bits.
 """
 import numpy as np
 import pytest
@@ -74,3 +76,36 @@ def test_noalloc_repeat_and_empty():
     assert torch.equal(Y1, Y2)
     m.apex4_w4a4_gemm_noalloc(d[0][:0], d[1][:0], d[2], d[3], G)
     torch.cuda.synchronize()
+
+
+def test_noalloc_graph_replay():
+    """The entry point's use case: captured in a graph (split over K, and the
+    few-row kernel's stream-K form, both on the static scratch), replayed
+    three times with eager calls between; every replay gives the eager bits."""
+    import torch
+    m = pk()
+    cases = [(256, 8192, 8192, 128), (16, 1024, 8192, 32)]
+    ins, eager = [], []
+    for (M, N, K, G) in cases:
+        r = np.random.default_rng(M + N + K + G)
+        d = [dev(a) for a in (wl.random_codes(r, M, K), wl.random_scales(r, M, K // G),
+                              wl.random_codes(r, N, K), wl.random_scales(r, N, K // G))]
+        ins.append(d)
+        eager.append(m.apex4_w4a4_gemm_noalloc(*d, G))
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        outs = [m.apex4_w4a4_gemm_noalloc(*d, c[3]) for d, c in zip(ins, cases)]
+    torch.cuda.synchronize()
+    for i in range(3):
+        for y in outs:
+            y.fill_(float("nan"))
+        for d, c in zip(ins, cases):                 # eager calls on the same scratch between replays
+            m.apex4_w4a4_gemm_noalloc(*d, c[3])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for y, e in zip(outs, eager):
+            assert torch.equal(y, e), i
