@@ -115,7 +115,7 @@ def test_pingpong_equals_general_tiles(O, paper):
 # ragged shapes on 128 x 256 tiles (G = 128, and G = 256: two stages per
 # group), and split-K shapes (G = 128)
 PP_SHAPES = [(1111, 8200, 640, 128), (1500, 8195, 1152, 128), (2050, 4100, 4096, 128), (4096, 4096, 1024, 128),
-             (1111, 8200, 1280, 256), (2050, 4100, 4096, 256), (4096, 4096, 512, 256)]
+             (1111, 8200, 1280, 256), (2050, 4100, 4096, 256), (4096, 4096, 512, 256), (2048, 4096, 28672, 256)]
 PP_SPLIT = [(256, 8192, 8192, 128), (512, 4096, 8192, 128), (300, 2000, 4096, 128)]
 
 
