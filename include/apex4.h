@@ -136,7 +136,8 @@ int apex4_w4a4_gemm_groupsums(const uint8_t* A_q, const uint8_t* W_q,
                               int64_t M, int64_t N, int64_t K, int64_t G,
                               int64_t m0, int64_t mr, int32_t* P, void* stream);
 
-/* flags of apex4_w4a4_gemm_debug (and of apex4_w4a4_gemm_plan, apex4_w4a4_linear_debug) */
+/* flags of apex4_w4a4_gemm_debug (and of apex4_w4a4_gemm_plan, apex4_w4a4_linear_debug,
+   apex4_w4a4_linear_ws) */
 #define APEX4_DEBUG_GENERAL_TILES 1 /* tile kernel only: no one-row, few-row or ping-pong (G = 128, 256) kernel */
 #define APEX4_DEBUG_W_TILED 2       /* W_q is in the tiled layout of apex4_tile_weights */
 
@@ -167,6 +168,7 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
 #define APEX4_ENTRY_GEMM 0    /* apex4_w4a4_gemm (and _debug without workspace) */
 #define APEX4_ENTRY_GEMM_WS 1 /* apex4_w4a4_gemm_ws (and _debug with workspace) */
 #define APEX4_ENTRY_LINEAR 2  /* apex4_w4a4_linear (and _debug); its GEMM, after the quantizer */
+#define APEX4_ENTRY_LINEAR_WS 3 /* apex4_w4a4_linear_ws; its GEMM, after the quantizer */
 #define APEX4_KERNEL_GEMV 1       /* one row (two on tiled weights): v_dot8 on the packed codes */
 #define APEX4_KERNEL_FUSED 2      /* one row: quantizer fused into the GEMV's prologue */
 #define APEX4_KERNEL_DECODE 3     /* up to 32 rows: weights streamed once through the MFMA */
@@ -177,10 +179,10 @@ int apex4_w4a4_gemm_debug(const uint8_t* A_q, const void* s_a,
 
 /*
  * The GEMM kernel that `entry` runs for this shape on the current device, and
- * its split over K (*splits = S > 1 only for APEX4_ENTRY_GEMM_WS, whose
- * workspace size query then returns S M N 4 bytes).  flags as in
+ * its split over K (*splits = S > 1 only for APEX4_ENTRY_GEMM_WS and
+ * APEX4_ENTRY_LINEAR_WS, whose workspace size query then returns S M N 4 bytes).  flags as in
  * apex4_w4a4_gemm_debug (APEX4_DEBUG_W_TILED: the tiled entry points;
- * APEX4_ENTRY_LINEAR takes no APEX4_DEBUG_GENERAL_TILES).  M == 0 gives kernel 0,
+ * APEX4_ENTRY_LINEAR and APEX4_ENTRY_LINEAR_WS take no APEX4_DEBUG_GENERAL_TILES).  M == 0 gives kernel 0,
  * splits 0.  Shape and group rules as apex4_w4a4_gemm; unknown entry or flags:
  * APEX4_ERR_SHAPE.  Launches nothing.
  */
@@ -247,6 +249,31 @@ int apex4_w4a4_linear(const void* x, const uint8_t* W_q, const void* s_w,
 int apex4_w4a4_linear_tiled(const void* x, const uint8_t* W_t, const void* s_w,
                             int64_t M, int64_t N, int64_t K, int64_t G,
                             void* Y, uint8_t* A_q_work, void* s_a_work, void* stream);
+
+/*
+ * Workspace form of apex4_w4a4_linear (flags 0: W row-major, W_q) and of
+ * apex4_w4a4_linear_tiled (flags APEX4_DEBUG_W_TILED: W in the tiled layout,
+ * W_t): the quantizer into the work buffers, then the GEMM with the kernel
+ * choice of apex4_w4a4_gemm_ws (tiled: apex4_w4a4_gemm_tiled given a
+ * workspace), i.e. split over K, or the few-row kernel's stream-K form, where
+ * those apply (Eq. (group_decomposition) split over K across workgroups).
+ * For one row where apex4_w4a4_linear fuses the quantizer into the GEMM, that
+ * fused kernel runs and takes no workspace.  Y and the work buffers end up
+ * exactly as after apex4_quantize_act followed by that GEMM entry point on the
+ * same stream.
+ *
+ *   x, W, s_w, Y, A_q_work, s_a_work: as apex4_w4a4_linear;
+ *   workspace: as apex4_w4a4_gemm_ws, at least apex4_w4a4_gemm_workspace_size
+ *   bytes for this shape (the same size for both weight layouts); may be NULL
+ *   where that size is 0.
+ * flags other than 0 and APEX4_DEBUG_W_TILED: APEX4_ERR_SHAPE.  Errors as
+ * apex4_w4a4_linear, plus APEX4_ERR_WORKSPACE when the workspace is needed and
+ * NULL or short; that check comes before any launch, so nothing is written.
+ */
+int apex4_w4a4_linear_ws(const void* x, const uint8_t* W, const void* s_w,
+                         int64_t M, int64_t N, int64_t K, int64_t G,
+                         void* Y, uint8_t* A_q_work, void* s_a_work,
+                         void* workspace, int64_t workspace_bytes, int flags, void* stream);
 
 /*
  * Debug form of apex4_w4a4_linear (flags 0) or apex4_w4a4_linear_tiled (flags

@@ -26,7 +26,7 @@ STATUS = {0: "APEX4_OK", -1: "APEX4_ERR_NULL", -2: "APEX4_ERR_SHAPE", -3: "APEX4
 APEX4_DEBUG_GENERAL_TILES = 1
 APEX4_DEBUG_W_TILED = 2
 APEX4_NOALLOC_SCRATCH_BYTES = 32 << 20
-ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2}
+ENTRY = {"gemm": 0, "gemm_ws": 1, "linear": 2, "linear_ws": 3}
 KERNELS = {0: None, 1: "gemv", 2: "fused", 3: "decode", 4: "tile64", 5: "tile128", 6: "pingpong",
            7: "decode_split"}
 
@@ -36,7 +36,7 @@ EXPORTED = ("apex4_quantize_act", "apex4_w4a4_gemm", "apex4_w4a4_gemm_groupsums"
             "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
             "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws", "apex4_status_string",
             "apex4_version", "apex4_tiled_weights_size", "apex4_tile_weights", "apex4_w4a4_gemm_tiled",
-            "apex4_w4a4_linear_tiled")
+            "apex4_w4a4_linear_tiled", "apex4_w4a4_linear_ws")
 
 _lib = None
 
@@ -68,6 +68,7 @@ def lib() -> ctypes.CDLL:
     L.apex4_tile_weights.argtypes = [P, I, I, P, P]
     L.apex4_w4a4_gemm_tiled.argtypes = [P, P, P, P, I, I, I, I, P, P, I, P]
     L.apex4_w4a4_linear_tiled.argtypes = [P, P, P, I, I, I, I, P, P, P, P]
+    L.apex4_w4a4_linear_ws.argtypes = [P, P, P, I, I, I, I, P, P, P, P, I, ctypes.c_int, P]
     L.apex4_pack_fp6.argtypes = [P, I, I, P, P]
     L.apex4_w4a4_gemm_workspace_size.argtypes = [I, I, I, I, P]
     L.apex4_quantize_mx.argtypes = [P, I, I, I, P, P, P]
@@ -82,7 +83,7 @@ def lib() -> ctypes.CDLL:
               "apex4_w4a4_gemm_fp6", "apex4_w4a4_gemm_workspace_size", "apex4_w4a4_gemm_ws",
               "apex4_w4a4_gemm_noalloc", "apex4_quantize_mx", "apex4_w4a4_gemm_mx",
               "apex4_w4a4_gemm_mx_workspace_size", "apex4_w4a4_gemm_mx_ws", "apex4_tiled_weights_size",
-              "apex4_tile_weights", "apex4_w4a4_gemm_tiled", "apex4_w4a4_linear_tiled"):
+              "apex4_tile_weights", "apex4_w4a4_gemm_tiled", "apex4_w4a4_linear_tiled", "apex4_w4a4_linear_ws"):
         getattr(L, f).restype = ctypes.c_int
     L.apex4_status_string.argtypes = [ctypes.c_int]
     L.apex4_status_string.restype = ctypes.c_char_p
@@ -254,8 +255,8 @@ def apex4_w4a4_linear(x, W_q, s_w, G: int, Y=None, A_q_work=None, s_a_work=None,
 
 
 def apex4_w4a4_gemm_plan(entry: str, M: int, N: int, K: int, G: int, flags: int = 0):
-    """(kernel name, splits) that the entry point ("gemm", "gemm_ws" or
-    "linear") runs for this shape on the current device."""
+    """(kernel name, splits) that the entry point ("gemm", "gemm_ws", "linear"
+    or "linear_ws") runs for this shape on the current device."""
     k, s = ctypes.c_int(0), ctypes.c_int(0)
     _check("apex4_w4a4_gemm_plan", lib().apex4_w4a4_gemm_plan(ENTRY[entry], M, N, K, G, flags, ctypes.byref(k),
                                                               ctypes.byref(s)))
@@ -338,6 +339,33 @@ def apex4_w4a4_linear_tiled(x, W_t, s_w, G: int, Y=None, A_q_work=None, s_a_work
                                        _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
                                        _stream(x, stream))
     _check("apex4_w4a4_linear_tiled", rc)
+    return Y
+
+
+def apex4_w4a4_linear_ws(x, W, s_w, G: int, workspace=None, tiled: bool = False, Y=None, A_q_work=None,
+                         s_a_work=None, stream=None):
+    """apex4_w4a4_linear (tiled=True: apex4_w4a4_linear_tiled) with the GEMM
+    split over K, or in its stream-K form, where apex4_w4a4_gemm_ws would be;
+    workspace is a uint8 device tensor of at least
+    apex4_w4a4_gemm_workspace_size bytes (made here when None).  N from s_w."""
+    import torch
+    M, K = x.shape
+    N = s_w.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    if A_q_work is None:
+        A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if s_a_work is None:
+        s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
+    if workspace is None:
+        need = apex4_w4a4_gemm_workspace_size(M, N, K, G)
+        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=x.device)
+    rc = lib().apex4_w4a4_linear_ws(_dev(x, torch.float16, "x"), _dev(W, torch.uint8, "W"),
+                                    _dev(s_w, torch.float16, "s_w"), M, N, K, G, _dev(Y, torch.float16, "Y"),
+                                    _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
+                                    _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+                                    APEX4_DEBUG_W_TILED if tiled else 0, _stream(x, stream))
+    _check("apex4_w4a4_linear_ws", rc)
     return Y
 
 

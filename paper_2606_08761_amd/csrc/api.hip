@@ -364,6 +364,33 @@ int apex4_w4a4_linear_tiled(const void* x, const uint8_t* W_t, const void* s_w, 
     return linear_dispatch(x, W_t, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), true, stream);
 }
 
+int apex4_w4a4_linear_ws(const void* x, const uint8_t* W, const void* s_w, int64_t M, int64_t N, int64_t K,
+                         int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, void* workspace,
+                         int64_t workspace_bytes, int flags, void* stream) {
+    int rc = check_linear_args(x, W, s_w, M, N, K, G, Y, A_q_work, s_a_work);
+    if (rc) return rc;
+    if (flags & ~APEX4_DEBUG_W_TILED) return APEX4_ERR_SHAPE;
+    const bool wt = flags != 0;
+    if (wt && (rc = check_tiled(N, K, G))) return rc;
+    if (workspace && !aligned16(workspace)) return APEX4_ERR_ALIGN;
+    rc = check_device();
+    if (rc) return rc;
+    if (M == 0) return APEX4_OK;
+    // the workspace is checked before the quantizer runs, so that a refused
+    // call writes nothing (the fused one-row kernel takes none)
+    if (!apex4::fused_linear_fits(M, N, K, G, wt)) {
+        const int64_t need = apex4::splitk_workspace_bytes(M, N, K, G);
+        if (need > 0 && (!workspace || workspace_bytes < need)) return APEX4_ERR_WORKSPACE;
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        const hipError_t e = apex4::launch_quantize(static_cast<const uint16_t*>(x), M, K, G, A_q_work,
+                                                    static_cast<uint16_t*>(s_a_work), st);
+        if (e != hipSuccess) return APEX4_ERR_LAUNCH;
+        return gemm_dispatch(A_q_work, s_a_work, W, s_w, M, N, K, G, Y, need > 0 ? workspace : nullptr,
+                             workspace_bytes, apex4::Dump(), false, wt, stream);
+    }
+    return linear_dispatch(x, W, s_w, M, N, K, G, Y, A_q_work, s_a_work, apex4::Dump(), wt, stream);
+}
+
 int apex4_w4a4_linear_debug(const void* x, const uint8_t* W_q, const void* s_w, int64_t M, int64_t N, int64_t K,
                             int64_t G, void* Y, uint8_t* A_q_work, void* s_a_work, int64_t m0, int64_t mr, int32_t* P,
                             int flags, void* stream) {
@@ -389,9 +416,10 @@ int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, 
     if (rc) return rc;
     rc = check_gemm_group(K, G);
     if (rc) return rc;
-    if (entry < APEX4_ENTRY_GEMM || entry > APEX4_ENTRY_LINEAR) return APEX4_ERR_SHAPE;
+    if (entry < APEX4_ENTRY_GEMM || entry > APEX4_ENTRY_LINEAR_WS) return APEX4_ERR_SHAPE;
     if (flags & ~(APEX4_DEBUG_GENERAL_TILES | APEX4_DEBUG_W_TILED)) return APEX4_ERR_SHAPE;
-    if (entry == APEX4_ENTRY_LINEAR && (flags & APEX4_DEBUG_GENERAL_TILES)) return APEX4_ERR_SHAPE;
+    const bool linear = entry == APEX4_ENTRY_LINEAR || entry == APEX4_ENTRY_LINEAR_WS;
+    if (linear && (flags & APEX4_DEBUG_GENERAL_TILES)) return APEX4_ERR_SHAPE;
     const bool wt = (flags & APEX4_DEBUG_W_TILED) != 0;
     if (wt && (rc = check_tiled(N, K, G))) return rc;
     rc = check_device();
@@ -401,13 +429,14 @@ int apex4_w4a4_gemm_plan(int entry, int64_t M, int64_t N, int64_t K, int64_t G, 
         *splits = 0;
         return APEX4_OK;
     }
-    if (entry == APEX4_ENTRY_LINEAR && apex4::fused_linear_fits(M, N, K, G, wt)) {
+    if (linear && apex4::fused_linear_fits(M, N, K, G, wt)) {
         *kernel = apex4::kKernelFused;
         *splits = 1;
         return APEX4_OK;
     }
     const apex4::GemmPlan plan =
-        apex4::plan_gemm(M, N, K, G, entry == APEX4_ENTRY_GEMM_WS, (flags & APEX4_DEBUG_GENERAL_TILES) != 0, wt);
+        apex4::plan_gemm(M, N, K, G, entry == APEX4_ENTRY_GEMM_WS || entry == APEX4_ENTRY_LINEAR_WS,
+                         (flags & APEX4_DEBUG_GENERAL_TILES) != 0, wt);
     *kernel = plan.kernel;
     *splits = plan.splits;
     return APEX4_OK;

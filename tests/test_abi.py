@@ -202,7 +202,8 @@ def test_plan_validation(L):
     assert f(0, 8, 8, 256, 128, 0, None, ctypes.byref(sp)) == -1
     assert f(0, 8, 8, 48, 48, 0, ctypes.byref(k), ctypes.byref(sp)) == -2
     assert f(0, 8, 8, 65568, 65568, 0, ctypes.byref(k), ctypes.byref(sp)) == -3
-    assert f(3, 8, 8, 256, 128, 0, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown entry
+    assert f(4, 8, 8, 256, 128, 0, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown entry
+    assert f(3, 8, 8, 256, 128, 1, ctypes.byref(k), ctypes.byref(sp)) == -2   # nor for the workspace linear
     assert f(0, 8, 8, 256, 128, 4, ctypes.byref(k), ctypes.byref(sp)) == -2   # unknown flag
     assert f(2, 8, 8, 256, 128, 1, ctypes.byref(k), ctypes.byref(sp)) == -2   # no general tiles for the linear
     assert f(0, 8, 8, 256, 64, 2, ctypes.byref(k), ctypes.byref(sp)) == -3    # tiled needs G >= 128
@@ -220,6 +221,22 @@ def test_linear_validation(L):
     assert f(*args(), 4, 8, 384, 96, h.ptr(), h.ptr(), h.ptr(), s) == -3
     assert f(*args(x=h.ptr(2)), 4, 8, 96, 32, h.ptr(), h.ptr(), h.ptr(), s) == -4   # K = 96 accepted
     assert f(*args(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), s) == -4
+
+
+def test_linear_ws_validation(L):
+    h = Host()
+    f = L.apex4_w4a4_linear_ws
+    s = NULL
+    w = lambda **kw: [kw.get(k, h.ptr()) for k in ("x", "w", "sw")]
+    tail = lambda ws=None, flags=0: [h.ptr() if ws is None else ws, 1 << 20, flags, s]
+    assert f(*w(x=NULL), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), *tail()) == -1
+    assert f(*w(), 4, 8, 256, 128, h.ptr(), NULL, h.ptr(), *tail()) == -1
+    assert f(*w(), 4, 8, 200, 128, h.ptr(), h.ptr(), h.ptr(), *tail()) == -2
+    assert f(*w(), 4, 8, 384, 96, h.ptr(), h.ptr(), h.ptr(), *tail()) == -3
+    assert f(*w(), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), *tail(flags=1)) == -2    # only the tiled flag
+    assert f(*w(), 4, 8, 256, 64, h.ptr(), h.ptr(), h.ptr(), *tail(flags=2)) == -3     # tiled needs G >= 128
+    assert f(*w(x=h.ptr(2)), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), *tail()) == -4
+    assert f(*w(), 4, 8, 256, 128, h.ptr(), h.ptr(), h.ptr(), *tail(ws=h.ptr(8))) == -4  # misaligned workspace
 
 
 def test_fp6_validation(L):
@@ -315,6 +332,7 @@ b = np.zeros(1 << 16, np.uint8); p = ctypes.c_void_p((b.ctypes.data + 255) & ~25
 print(L.apex4_w4a4_gemm(p, p, p, p, 0, 8, 256, 128, p, None))
 k = ctypes.c_int(0)
 print(L.apex4_w4a4_gemm_plan(0, 8, 8, 96, 32, 0, ctypes.byref(k), ctypes.byref(k)))
+print(L.apex4_w4a4_linear_ws(p, p, p, 4, 8, 256, 128, p, p, p, None, 0, 0, None))
 """ % ROOT
     try:
         import torch
@@ -324,7 +342,7 @@ print(L.apex4_w4a4_gemm_plan(0, 8, 8, 96, 32, 0, ctypes.byref(k), ctypes.byref(k
         pass
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
     assert out.returncode == 0, out.stderr
-    assert out.stdout.strip().splitlines()[-2:] == ["-6", "-6"]
+    assert out.stdout.strip().splitlines()[-3:] == ["-6", "-6", "-6"]
 
 
 def test_binding_refuses_host_tensors():
