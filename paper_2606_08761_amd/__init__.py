@@ -347,7 +347,8 @@ def apex4_w4a4_linear_ws(x, W, s_w, G: int, workspace=None, tiled: bool = False,
     """apex4_w4a4_linear (tiled=True: apex4_w4a4_linear_tiled) with the GEMM
     split over K, or in its stream-K form, where apex4_w4a4_gemm_ws would be;
     workspace is a uint8 device tensor of at least
-    apex4_w4a4_gemm_workspace_size bytes (made here when None).  N from s_w."""
+    apex4_w4a4_gemm_workspace_size bytes (when None: made here if the shape
+    needs one, else none is passed).  N from s_w."""
     import torch
     M, K = x.shape
     N = s_w.shape[0]
@@ -357,13 +358,15 @@ def apex4_w4a4_linear_ws(x, W, s_w, G: int, workspace=None, tiled: bool = False,
         A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
     if s_a_work is None:
         s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
-    if workspace is None:
+    if workspace is None and M:
         need = apex4_w4a4_gemm_workspace_size(M, N, K, G)
-        workspace = torch.empty((max(need, 16),), dtype=torch.uint8, device=x.device)
+        if need:
+            workspace = torch.empty((need,), dtype=torch.uint8, device=x.device)
+    ws = ctypes.c_void_p(0) if workspace is None else _dev(workspace, torch.uint8, "workspace")
     rc = lib().apex4_w4a4_linear_ws(_dev(x, torch.float16, "x"), _dev(W, torch.uint8, "W"),
                                     _dev(s_w, torch.float16, "s_w"), M, N, K, G, _dev(Y, torch.float16, "Y"),
                                     _dev(A_q_work, torch.uint8, "A_q_work"), _dev(s_a_work, torch.float16, "s_a_work"),
-                                    _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+                                    ws, 0 if workspace is None else workspace.numel(),
                                     APEX4_DEBUG_W_TILED if tiled else 0, _stream(x, stream))
     _check("apex4_w4a4_linear_ws", rc)
     return Y
@@ -533,15 +536,10 @@ class W4A4Linear:
                 Y = apex4_w4a4_gemm_mx(Aq, sa, self.W_q, self.s_w, self.G, stream=stream)
             else:
                 Y = apex4_w4a4_gemm_mx_ws(Aq, sa, self.W_q, self.s_w, self.G, ws, stream=stream)
-        elif self.tiled:
-            if ws is None:
-                Y = apex4_w4a4_linear_tiled(x2, self.W_t, self.s_w, self.G, None, Aq, sa, stream=stream)
-            else:
-                apex4_quantize_act(x2, self.G, Aq, sa, stream=stream)
-                Y = apex4_w4a4_gemm_tiled(Aq, sa, self.W_t, self.s_w, self.G, ws, stream=stream)
-        elif ws is None:
-            Y = apex4_w4a4_linear(x2, self.W_q, self.s_w, self.G, None, Aq, sa, stream=stream)
         else:
-            apex4_quantize_act(x2, self.G, Aq, sa, stream=stream)
-            Y = apex4_w4a4_gemm_ws(Aq, sa, self.W_q, self.s_w, self.G, ws, stream=stream)
+            # one C call: the quantizer, then the GEMM (split over K or stream-K
+            # where the cached workspace exists; fused for one row where it pays)
+            W = self.W_t if self.tiled else self.W_q
+            Y = apex4_w4a4_linear_ws(x2, W, self.s_w, self.G, workspace=ws, tiled=self.tiled, A_q_work=Aq,
+                                     s_a_work=sa, stream=stream)
         return Y.reshape(*lead, self.N)
