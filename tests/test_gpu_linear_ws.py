@@ -113,3 +113,27 @@ def test_linear_ws_refuses_a_missing_workspace_before_writing(M, N, K, G):
         assert rc == -7, rc
     torch.cuda.synchronize()
     assert bool((Aw == 0xAB).all()) and bool((sa == 3.0).all()) and bool((Y == 7.0).all())
+
+
+@pytest.mark.parametrize("tiled", [False, True])
+def test_linear_ws_zero_and_two_rows(O, tiled):
+    """M = 0 is a no-op; M = 2 (the dot-product kernel on tiled weights, the
+    few-row kernel on row-major ones) equals the quantizer plus that GEMM."""
+    import torch
+    m = pk()
+    N, K, G = 264, 4096, 128
+    w = wl.weights(wl.rng_for("decode", 53, N + K), N, K)
+    Wq, sw = m.apex4_quantize_act(dev(w), G)
+    W = m.apex4_tile_weights(Wq) if tiled else Wq
+    Y0 = m.apex4_w4a4_linear_ws(torch.empty((0, K), dtype=torch.float16, device="cuda"), W, sw, G, tiled=tiled)
+    assert Y0.shape == (0, N)
+    x = wl.activations(wl.rng_for("decode", 54, K), 2, K)
+    xd = dev(x)
+    Y = m.apex4_w4a4_linear_ws(xd, W, sw, G, tiled=tiled)
+    Aq, sa = m.apex4_quantize_act(xd, G)
+    Y2 = m.apex4_w4a4_gemm_tiled(Aq, sa, W, sw, G) if tiled else m.apex4_w4a4_gemm_ws(Aq, sa, W, sw, G)
+    torch.cuda.synchronize()
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+    Aq_o, sa_o = O.quantize(x, G)
+    Wq_o, sw_o = O.quantize(w, G)
+    check_tolerance(host(Y), O.gemm_rows(Aq_o, sa_o, Wq_o, sw_o, K, G), f"linear_ws 2 rows tiled={tiled}")
