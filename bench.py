@@ -439,14 +439,15 @@ def decode_split_mode(reps: int = 40, rounds: int = 6):
 def layers_mode(reps: int = 10):
     """The linears of one Llama-2-70B decoder layer under the uniform G=128 and the
     mixed configuration, each linear timed as quantize + W4A4 GEMM from fp16
-    activations (apex4_w4a4_linear), next to fp16 GEMMs of the same shapes
+    activations (apex4_w4a4_linear_ws), next to fp16 GEMMs of the same shapes
     (torch.matmul -> hipBLASLt).  Weights are rotated over at least 512 MB of
     copies (twice the Infinity Cache); codes and scales are random (speed does
     not depend on values).  The W4A4 linears are timed from a replayed graph of
     `reps` calls (GPU time, no Python launch overhead), the fp16 GEMMs eagerly.
     Each linear runs as W4A4Linear runs it: weights in the tiled layout for
-    G >= 128 (row-major below), the linear entry point, or the quantizer
-    followed by the GEMM split over K with a workspace where that applies."""
+    G >= 128 (row-major below), one apex4_w4a4_linear_ws call (the quantizer,
+    then the GEMM, split over K or stream-K with a workspace where that
+    applies)."""
     import torch
     import paper_2606_08761_amd as pk
     from paper_2606_08761_amd import workloads as wl
@@ -509,19 +510,13 @@ def layers_mode(reps: int = 10):
                 ws = wsets[name]
                 need = pk.apex4_w4a4_gemm_workspace_size(Ml, Nl, Kl, Gv)
                 tiled = Gv >= 128
-                if need:
-                    # as W4A4Linear: quantize, then the GEMM split over K with a workspace
-                    work = torch.empty((need,), dtype=torch.uint8, device=dev)
-                    gemm = pk.apex4_w4a4_gemm_tiled if tiled else pk.apex4_w4a4_gemm_ws
+                # as W4A4Linear: one apex4_w4a4_linear_ws call (the quantizer, then
+                # the GEMM, split over K or stream-K where a workspace applies)
+                work = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
 
-                    def call(i):
-                        pk.apex4_quantize_act(x, Gv, Aq, sa)
-                        gemm(Aq, sa, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, work, Y)
-                else:
-                    linear = pk.apex4_w4a4_linear_tiled if tiled else pk.apex4_w4a4_linear
-
-                    def call(i):
-                        linear(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, Y, Aq, sa)
+                def call(i):
+                    pk.apex4_w4a4_linear_ws(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, workspace=work,
+                                            tiled=tiled, Y=Y, A_q_work=Aq, s_a_work=sa)
                 t = graph_timed(call, reps)
                 # the workspace's use: S K ranges on the tile kernels, or the
                 # stream-K form of the few-row kernel (reported as 0)
@@ -590,10 +585,10 @@ def summarize_layers(path, command):
     tot = {(r["config"], r["M"]): r for r in rows}
     lines = ["# Llama-2-70B decoder-layer linears: uniform G=128 vs mixed granularity vs fp16", "",
              "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
-             "Each W4A4 linear is timed as W4A4Linear runs it: quantize + GEMM from fp16 activations "
-             "(apex4_w4a4_linear_tiled on tiled weights for G >= 128, apex4_w4a4_linear on row-major weights "
-             "below; or, where the library asks for a workspace, the quantizer + the GEMM with it: split over K into S "
-             "ranges on the tile kernels, marked S=, or the few-row kernel's stream-K form, marked stream-K) "
+             "Each W4A4 linear is timed as W4A4Linear runs it: quantize + GEMM from fp16 activations in one "
+             "apex4_w4a4_linear_ws call (tiled weights for G >= 128, row-major below; where the library asks "
+             "for a workspace, the GEMM is split over K into S ranges on the tile kernels, marked S=, or runs "
+             "the few-row kernel's stream-K form, marked stream-K) "
              "from a replayed graph (GPU time), weights rotated over >= 512 MB of copies; fp16 is "
              "torch.matmul (hipBLASLt) on the same shapes, rotated the same way, timed eagerly. "
              "mix: G=32 for the value and down projections, per-channel (G=K) elsewhere; q and k "
