@@ -516,7 +516,7 @@ def layers_mode(reps: int = 10):
 
                 def call(i):
                     pk.apex4_w4a4_linear_ws(x, ws[i % len(ws)][0], ws[i % len(ws)][1], Gv, workspace=work,
-                                            tiled=tiled, Y=Y, A_q_work=Aq, s_a_work=sa)
+                                            tiled=tiled, Y=Y, A_q_work=Aq, s_a_work=sa, make_workspace=False)
                 t = graph_timed(call, reps)
                 # the workspace's use: S K ranges on the tile kernels, or the
                 # stream-K form of the few-row kernel (reported as 0)

@@ -343,12 +343,13 @@ def apex4_w4a4_linear_tiled(x, W_t, s_w, G: int, Y=None, A_q_work=None, s_a_work
 
 
 def apex4_w4a4_linear_ws(x, W, s_w, G: int, workspace=None, tiled: bool = False, Y=None, A_q_work=None,
-                         s_a_work=None, stream=None):
+                         s_a_work=None, stream=None, make_workspace: bool = True):
     """apex4_w4a4_linear (tiled=True: apex4_w4a4_linear_tiled) with the GEMM
     split over K, or in its stream-K form, where apex4_w4a4_gemm_ws would be;
     workspace is a uint8 device tensor of at least
-    apex4_w4a4_gemm_workspace_size bytes (when None: made here if the shape
-    needs one, else none is passed).  N from s_w."""
+    apex4_w4a4_gemm_workspace_size bytes.  When it is None: with
+    make_workspace, one is made here if the shape needs one; without, none is
+    passed (for callers that know the shape needs none).  N from s_w."""
     import torch
     M, K = x.shape
     N = s_w.shape[0]
@@ -358,7 +359,7 @@ def apex4_w4a4_linear_ws(x, W, s_w, G: int, workspace=None, tiled: bool = False,
         A_q_work = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
     if s_a_work is None:
         s_a_work = torch.empty((M, max(K // G, 1)), dtype=torch.float16, device=x.device)
-    if workspace is None and M:
+    if workspace is None and M and make_workspace:
         need = apex4_w4a4_gemm_workspace_size(M, N, K, G)
         if need:
             workspace = torch.empty((need,), dtype=torch.uint8, device=x.device)
@@ -541,5 +542,5 @@ class W4A4Linear:
             # where the cached workspace exists; fused for one row where it pays)
             W = self.W_t if self.tiled else self.W_q
             Y = apex4_w4a4_linear_ws(x2, W, self.s_w, self.G, workspace=ws, tiled=self.tiled, A_q_work=Aq,
-                                     s_a_work=sa, stream=stream)
+                                     s_a_work=sa, stream=stream, make_workspace=False)
         return Y.reshape(*lead, self.N)
