@@ -23,3 +23,26 @@ def test_help_lists_the_modes():
     assert r.returncode == 0
     for mode in ("bench", "counters", "decode_counters", "decode_split", "decode_sq", "gsweep", "layers", "summarize"):
         assert mode in r.stdout, mode
+
+
+def test_timing_event_failure_is_an_exception_the_bench_catches():
+    """Without a usable device, creating a fence-free timing event raises one of
+    the exceptions the timed loop falls back on (torch's events) instead of
+    crashing.  Run in a child process so the HIP runtime probe stays out of the
+    test process."""
+    code = (f"import sys; sys.path.insert(0, {ROOT!r}); import bench\n"
+            "try:\n"
+            "    bench.TimingEvent()\n"
+            "    print('created')\n"
+            "except (OSError, AttributeError, RuntimeError) as e:\n"
+            "    print('refused', type(e).__name__)\n")
+    try:
+        import torch
+        if torch.cuda.is_available():
+            import pytest
+            pytest.skip("a GPU is visible")
+    except ImportError:
+        pass
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().startswith("refused"), r.stdout
